@@ -1,0 +1,121 @@
+"""Write workloads/stripe_params.json: density-targeted per-head stripe parameters.
+
+Run from the repository root:  python -m workloads.make_stripe_params
+
+Densities are evaluated with the oracle only (``oracle.block_coordinates`` and
+``oracle.axis_condition``).  Because the stripe condition factors into a temporal and a
+spatial test on the block coordinates, the kept-tile count of a tuple is
+f_T . C . f_S + (tiles touching a global block), where C[dt, ds] counts ordered pairs of
+non-global blocks at distance (dt, ds); this is exact, and ``tests/test_workloads.py`` checks
+it against the oracle's full block map.
+
+* wan1_3b / wan14b / hunyuan: head h draws a target density rho_h ~ U[lo, hi] with
+  ``default_rng([1, config index])``; among all candidate tuples (paper ranges, widths
+  1..extent) within 0.5 % of the closest achievable density, one is drawn at random.
+* sweep: eight runs with every head forced to 5,10,20,30,50,70,90,100 %; head h uses
+  T_s = 1 + (h mod T') and S_s = S' - (h mod S') (periods from 1 to the full extent), and the
+  (T_w, T_o, S_w, S_o) closest to the target (seeded random tie break).
+"""
+import itertools
+import json
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import oracle  # noqa: E402
+from workloads.configs import CONFIGS, SWEEP_TARGETS  # noqa: E402
+from workloads.params import (S_OFFSETS, S_STRIDES, T_OFFSETS, T_STRIDES,  # noqa: E402
+                              coarse_extent)
+
+CONFIG_INDEX = {name: i for i, name in enumerate(CONFIGS)}
+
+
+def pair_histogram(cfg):
+    t, s, _, g = oracle.block_coordinates(cfg.frames, cfg.height, cfg.width, cfg.n_text, cfg.block)
+    tp, sp = coarse_extent(cfg)
+    tv, sv = t[~g], s[~g]
+    dt = (tv[None, :] - tv[:, None]).ravel() + (tp - 1)
+    ds = (sv[None, :] - sv[:, None]).ravel() + (sp - 1)
+    hist = np.zeros((2 * tp - 1, 2 * sp - 1), dtype=np.int64)
+    np.add.at(hist, (dt, ds), 1)
+    nb = t.shape[0]
+    n_global_tiles = nb * nb - int((~g).sum()) ** 2
+    return hist, n_global_tiles, nb
+
+
+def axis_table(extent, tuples):
+    d = np.arange(-(extent - 1), extent)
+    return np.array([oracle.axis_condition(d, w, o, s) for (w, o, s) in tuples], dtype=np.int64)
+
+
+def densities(cfg, t_tuples, s_tuples):
+    hist, n_glob, nb = pair_histogram(cfg)
+    tp, sp = coarse_extent(cfg)
+    ft = axis_table(tp, t_tuples)
+    fs = axis_table(sp, s_tuples)
+    return (ft @ hist @ fs.T + n_glob) / float(nb * nb)
+
+
+def targeted(cfg, seed):
+    tp, sp = coarse_extent(cfg)
+    t_tuples = list(itertools.product(range(1, tp + 1), T_OFFSETS, T_STRIDES))
+    s_tuples = list(itertools.product(range(1, sp + 1), S_OFFSETS, S_STRIDES))
+    rho = densities(cfg, t_tuples, s_tuples).ravel()
+    rng = np.random.default_rng(seed)
+    lo, hi = cfg.density_band
+    params, achieved = [], []
+    for _ in range(cfg.heads):
+        target = rng.uniform(lo, hi)
+        err = np.abs(rho - target)
+        pool = np.nonzero(err <= err.min() + 0.005)[0]
+        pick = int(rng.choice(pool))
+        ti, si = divmod(pick, len(s_tuples))
+        params.append(list(t_tuples[ti]) + list(s_tuples[si]))
+        achieved.append(float(rho[pick]))
+    return {"params": params, "density": achieved}
+
+
+def sweep(cfg, seed):
+    tp, sp = coarse_extent(cfg)
+    rng = np.random.default_rng(seed)
+    out = {}
+    for target in SWEEP_TARGETS:
+        params, achieved = [], []
+        for h in range(cfg.heads):
+            ts, ss = 1 + (h % tp), sp - (h % sp)
+            t_tuples = [(w, o, ts) for w in range(1, tp + 1) for o in T_OFFSETS]
+            s_tuples = [(w, o, ss) for w in range(1, sp + 1) for o in S_OFFSETS]
+            rho = densities(cfg, t_tuples, s_tuples).ravel()
+            err = np.abs(rho - target)
+            pool = np.nonzero(err == err.min())[0]
+            pick = int(rng.choice(pool))
+            ti, si = divmod(pick, len(s_tuples))
+            params.append(list(t_tuples[ti]) + list(s_tuples[si]))
+            achieved.append(float(rho[pick]))
+        out["%.2f" % target] = {"params": params, "density": achieved}
+    return out
+
+
+def build():
+    data = {}
+    for name in ("wan1_3b", "wan14b", "hunyuan"):
+        data[name] = targeted(CONFIGS[name], [1, CONFIG_INDEX[name]])
+    data["sweep"] = sweep(CONFIGS["sweep"], [1, CONFIG_INDEX["sweep"]])
+    return data
+
+
+if __name__ == "__main__":
+    data = build()
+    path = os.path.join(ROOT, "workloads", "stripe_params.json")
+    with open(path, "w") as f:
+        json.dump(data, f, indent=1)
+    for name in ("wan1_3b", "wan14b", "hunyuan"):
+        d = data[name]["density"]
+        print(name, "mean density %.4f  min %.4f  max %.4f" % (np.mean(d), min(d), max(d)))
+    for key, run in data["sweep"].items():
+        print("sweep", key, "mean density %.4f" % np.mean(run["density"]))
