@@ -1,0 +1,138 @@
+/*
+ * psa.h -- C ABI of libpsa: forward pass of PSA (Parameterized Stripe Attention) block-sparse
+ * spatio-temporal attention on AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper: "Parameterized Stripe Attention for Efficient Video Generation"):
+ *
+ *  - Sec. 3.2, "Unified Representation": every attention head carries six integers
+ *    M = (T_w, T_o, T_s, S_w, S_o, S_s): width, offset and stride of the inter-frame (temporal)
+ *    and intra-frame (spatial) diagonal stripes.
+ *  - Algorithm 1 (PSA mask definition): a query at frame t_q, in-frame position s_q may attend to
+ *    a key at (t_k, s_k) iff (|t_k - t_q - T_o| mod T_s) <= T_w - 1 and
+ *    (|s_k - s_q - S_o| mod S_s) <= S_w - 1.
+ *  - Sec. 3.2, "Hardware-Aware Design": the test is applied per (query block, key block) pair,
+ *    never per token.  Here a block is `block` consecutive tokens of the frame-major (t, h, w)
+ *    sequence; its coordinates are those of its first token: t = (b*block) div (H*W),
+ *    s = ((b*block) mod (H*W)) div block.  Temporal parameters therefore count frames and
+ *    spatial parameters count block slots within a frame.  Text tokens appended after the
+ *    F*H*W video tokens are global: a block holding any text token is kept in its whole row and
+ *    column.
+ *  - Algorithm 2 (PSA-Kernel): for each query block, only the kept key/value blocks are visited;
+ *    S = Q K^T, keys past the end of the sequence get -inf, safe (online) softmax, O += P V.
+ *
+ * Conventions shared by every call:
+ *  - Tensors are bf16, contiguous, layout [batch][n_heads][N][head_dim] (row-major).
+ *  - Tensor pointers are device pointers owned by the caller; nothing is retained after the
+ *    call.  `params` is a host array of n_heads entries, read before the call returns.
+ *  - Every call only enqueues work on `stream` (0 = the null stream of the current device) and
+ *    returns; results are ready after the caller synchronises that stream.  The current device
+ *    must be the stream's device.
+ *  - Arguments are validated before anything is enqueued: on PSA_ERR_INVALID,
+ *    PSA_ERR_UNSUPPORTED or PSA_ERR_WORKSPACE no output byte is written.  PSA_ERR_HIP reports a
+ *    failed HIP call (launch); psa_last_error() then holds the HIP message.
+ *  - The library holds no allocation and no mutable global state apart from the thread-local
+ *    error message; calls are re-entrant.  Two calls that share an output or a workspace must
+ *    not overlap in time.
+ *  - Numerics: bf16 x bf16 products accumulated in fp32 (MFMA); softmax statistics in fp32;
+ *    P rounded to bf16 before P V; O rounded to bf16 (round to nearest even).  A query row with
+ *    no kept key gets O = 0 and LSE = -inf.
+ */
+#ifndef PSA_H
+#define PSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Stride meaning "a single diagonal" (paper appendix on candidate initialisation: an infinite
+ * stride leaves one diagonal; any stride >= the axis extent plus |offset| behaves the same). */
+#define PSA_STRIDE_INF 0x7fffffff
+
+/* Largest |offset| accepted. */
+#define PSA_MAX_OFFSET (1 << 24)
+
+/* Largest number of blocks per sequence accepted by psa_attention_fwd. */
+#define PSA_MAX_BLOCKS 8192
+
+/* Largest batch * n_heads accepted by psa_attention_fwd (scheduler limit). */
+#define PSA_MAX_BATCH_HEADS 4096
+
+/* M(T_w, T_o, T_s, S_w, S_o, S_s) of one head (Sec. 3.2).  Widths and strides must be >= 1. */
+typedef struct {
+  int32_t t_w, t_o, t_s;
+  int32_t s_w, s_o, s_s;
+} psa_stripe_t;
+
+/* Latent video grid F x H x W (frame-major) followed by n_text text tokens:
+ * N = frames * height * width + n_text. */
+typedef struct {
+  int32_t frames, height, width, n_text;
+} psa_grid_t;
+
+typedef enum {
+  PSA_OK = 0,
+  PSA_ERR_INVALID = 1,     /* null pointer, width/stride < 1, |offset| too large, bad sizes */
+  PSA_ERR_UNSUPPORTED = 2, /* head_dim or block outside {64, 128}, too many blocks or heads */
+  PSA_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than psa_workspace_size() */
+  PSA_ERR_HIP = 4          /* a HIP runtime call failed; see psa_last_error() */
+} psa_status_t;
+
+/* Number of blocks ceil(N / block) of the grid, or -1 if grid or block is invalid. */
+int32_t psa_num_blocks(psa_grid_t grid, int32_t block);
+
+/* Bytes of device workspace psa_attention_fwd needs for these sizes (0 if invalid).
+ * The workspace holds the decoded per-head parameters, the kept-block count of every
+ * (batch, head, query block) work item, the load-balanced work order and queue counters. */
+size_t psa_workspace_size(int32_t batch, int32_t n_heads, psa_grid_t grid, int32_t block);
+
+/* Block map of Algorithm 1 at block granularity (Sec. 3.2), computed on the device by the same
+ * decoder that psa_attention_fwd runs inside its kernels.  block >= 1 (block = 1 evaluates
+ * Algorithm 1 token by token).  Any output may be NULL (not written):
+ *   blockmap      device uint8 [n_heads][nb][nb]; row = query block, column = key block; 1 = kept
+ *   kept_per_row  device int32 [n_heads][nb]: kept key blocks of each query block
+ *   kept_per_head device int64 [n_heads]: kept tiles of each head
+ * with nb = psa_num_blocks(grid, block). */
+psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa_grid_t grid,
+                                int32_t block, uint8_t* blockmap, int32_t* kept_per_row,
+                                int64_t* kept_per_head, hipStream_t stream);
+
+/* PSA block-sparse attention forward (Algorithm 2): o = softmax(scale * q k^T restricted to the
+ * kept blocks of each head) v.
+ *   q, k, v, o     device bf16 [batch][n_heads][N][head_dim]; N = frames*height*width + n_text
+ *   head_dim       64 or 128;  block: 64 or 128 (query and key block size, the tile size)
+ *   params         host [n_heads]; the same M for every batch element
+ *   softmax_scale  multiplies q.k before the softmax (typically 1/sqrt(head_dim))
+ *   workspace      device, at least psa_workspace_size(batch, n_heads, grid, block) bytes,
+ *                  256-byte aligned; contents on entry are ignored and are clobbered
+ *   lse            device fp32 [batch][n_heads][N] (natural-log softmax normaliser), or NULL
+ *   kept_per_row   device int32 [n_heads][nb]: the kept-block counts decoded for the schedule,
+ *                  or NULL */
+psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void* o,
+                               int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
+                               int32_t block, const psa_stripe_t* params, float softmax_scale,
+                               void* workspace, size_t workspace_bytes, float* lse,
+                               int32_t* kept_per_row, hipStream_t stream);
+
+/* Dense attention forward with the same tile engine (every block kept): the speedup baseline.
+ * Same tensor layout, with N = n_tokens.  At full density psa_attention_fwd returns the same
+ * bits as this call. */
+psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o, int32_t batch,
+                           int32_t n_heads, int32_t head_dim, int32_t n_tokens, int32_t block,
+                           float softmax_scale, float* lse, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* psa_status_string(psa_status_t status);
+
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+const char* psa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PSA_H */

@@ -1,0 +1,154 @@
+"""PSA (Parameterized Stripe Attention) block-sparse attention forward for MI355X (gfx950).
+
+Thin torch-facing wrapper around the C ABI of ``libpsa.so`` (``include/psa.h``): tensors are
+only checked for dtype, device and layout, then their device pointers and the current HIP
+stream are handed to the library.  Every computation runs in the library's HIP kernels; there
+is no CPU or PyTorch fallback.
+
+    params = [(T_w, T_o, T_s, S_w, S_o, S_s), ...]          # one 6-tuple per head
+    o = attention_fwd(q, k, v, grid=(F, H, W, n_text), block=128, params=params)
+    o_dense = dense_fwd(q, k, v, block=128)
+    bmap, per_row, per_head = build_blockmap(params, (F, H, W, n_text), block=128)
+"""
+import math
+
+from . import _lib
+from ._lib import STRIDE_INF, PsaError  # noqa: F401
+
+__all__ = ["STRIDE_INF", "PsaError", "num_blocks", "workspace_size", "build_blockmap",
+           "attention_fwd", "dense_fwd", "Workspace", "library_path"]
+
+
+def library_path():
+    return _lib.LIB_PATH
+
+
+def _grid(grid):
+    g = tuple(int(x) for x in grid)
+    if len(g) == 3:
+        g = g + (0,)
+    if len(g) != 4:
+        raise ValueError("grid is (frames, height, width[, n_text])")
+    return _lib.grid_of(*g)
+
+
+def num_blocks(grid, block):
+    return int(_lib.lib().psa_num_blocks(_grid(grid), int(block)))
+
+
+def workspace_size(batch, n_heads, grid, block):
+    return int(_lib.lib().psa_workspace_size(int(batch), int(n_heads), _grid(grid), int(block)))
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream, device):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes_void(stream.cuda_stream)
+
+
+def ctypes_void(x):
+    import ctypes
+    return ctypes.c_void_p(int(x)) if x else None
+
+
+def _ptr(t):
+    return ctypes_void(t.data_ptr()) if t is not None else None
+
+
+def _check_qkv(*ts):
+    torch = _torch()
+    ref = ts[0]
+    for t in ts:
+        if t.dtype != torch.bfloat16:
+            raise TypeError("q, k, v must be bfloat16")
+        if not t.is_cuda:
+            raise ValueError("q, k, v must be GPU tensors")
+        if not t.is_contiguous():
+            raise ValueError("q, k, v must be contiguous [batch, heads, N, head_dim]")
+        if t.dim() != 4 or t.shape != ref.shape:
+            raise ValueError("q, k, v must share the shape [batch, heads, N, head_dim]")
+        if t.device != ref.device:
+            raise ValueError("q, k, v must be on one device")
+
+
+class Workspace:
+    """Device workspace for attention_fwd (a byte tensor on the given device)."""
+
+    def __init__(self, batch, n_heads, grid, block, device):
+        torch = _torch()
+        self.nbytes = workspace_size(batch, n_heads, grid, block)
+        if self.nbytes == 0:
+            raise ValueError("invalid sizes for a workspace")
+        self.tensor = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+
+
+def build_blockmap(params, grid, block, device=None, blockmap=True, per_row=True, per_head=True,
+                   stream=None):
+    """Block map of the stripe parameters on the device.
+
+    Returns (map uint8 [heads, nb, nb] | None, kept_per_row int32 [heads, nb] | None,
+    kept_per_head int64 [heads] | None)."""
+    torch = _torch()
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    heads = len(params)
+    nb = num_blocks(grid, block)
+    if nb < 0:
+        raise ValueError("invalid grid or block")
+    bm = torch.empty((heads, nb, nb), dtype=torch.uint8, device=device) if blockmap else None
+    pr = torch.empty((heads, nb), dtype=torch.int32, device=device) if per_row else None
+    ph = torch.empty((heads,), dtype=torch.int64, device=device) if per_head else None
+    with torch.cuda.device(device):
+        _lib.check(_lib.lib().psa_build_blockmap(_lib.stripes(params), heads, _grid(grid), int(block),
+                                                 _ptr(bm), _ptr(pr), _ptr(ph), _stream(stream, device)))
+    return bm, pr, ph
+
+
+def attention_fwd(q, k, v, grid, block, params, scale=None, out=None, return_lse=False,
+                  workspace=None, return_kept_per_row=False, stream=None):
+    """PSA block-sparse attention forward.  q, k, v: bf16 [batch, heads, N, head_dim], contiguous.
+
+    Returns o (and lse float32 [batch, heads, N], kept_per_row int32 [heads, nb] if asked)."""
+    torch = _torch()
+    _check_qkv(q, k, v)
+    b, h, n, d = q.shape
+    if len(params) != h:
+        raise ValueError("one stripe tuple per head is required")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q) if out is None else out
+    _check_qkv(q, o)
+    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+    nb = num_blocks(grid, block)
+    kept = torch.empty((h, max(nb, 1)), dtype=torch.int32, device=q.device) if return_kept_per_row else None
+    ws = workspace if workspace is not None else Workspace(b, h, grid, block, q.device)
+    with torch.cuda.device(q.device):
+        _lib.check(_lib.lib().psa_attention_fwd(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, _grid(grid), int(block),
+            _lib.stripes(params), scale, _ptr(ws.tensor), ws.nbytes, _ptr(lse), _ptr(kept),
+            _stream(stream, q.device)))
+    res = (o,)
+    if return_lse:
+        res += (lse,)
+    if return_kept_per_row:
+        res += (kept,)
+    return res[0] if len(res) == 1 else res
+
+
+def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=None):
+    """Dense attention forward with the same tile engine (the speedup baseline)."""
+    torch = _torch()
+    _check_qkv(q, k, v)
+    b, h, n, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q) if out is None else out
+    _check_qkv(q, o)
+    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+    with torch.cuda.device(q.device):
+        _lib.check(_lib.lib().psa_dense_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, n, int(block),
+                                            scale, _ptr(lse), _stream(stream, q.device)))
+    return (o, lse) if return_lse else o

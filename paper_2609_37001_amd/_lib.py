@@ -1,0 +1,98 @@
+"""ctypes binding of libpsa.so (include/psa.h).  Argument marshalling only: every step of the
+attention path runs in the HIP kernels of the library; torch supplies device memory and streams.
+
+The library is loaded from this package directory; if it is missing the import of the binding
+functions raises, there is no fallback.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libpsa.so")
+
+STRIDE_INF = 0x7FFFFFFF
+MAX_OFFSET = 1 << 24
+MAX_BLOCKS = 8192
+MAX_BATCH_HEADS = 4096
+
+PSA_OK = 0
+PSA_ERR_INVALID = 1
+PSA_ERR_UNSUPPORTED = 2
+PSA_ERR_WORKSPACE = 3
+PSA_ERR_HIP = 4
+
+EXPORTS = ("psa_num_blocks", "psa_workspace_size", "psa_build_blockmap", "psa_attention_fwd",
+           "psa_dense_fwd", "psa_status_string", "psa_last_error")
+
+
+class Stripe(ctypes.Structure):
+    _fields_ = [("t_w", ctypes.c_int32), ("t_o", ctypes.c_int32), ("t_s", ctypes.c_int32),
+                ("s_w", ctypes.c_int32), ("s_o", ctypes.c_int32), ("s_s", ctypes.c_int32)]
+
+
+class Grid(ctypes.Structure):
+    _fields_ = [("frames", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("n_text", ctypes.c_int32)]
+
+
+class PsaError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__("%s (%s)" % (detail, _status_name(status)))
+        self.status = status
+
+
+_STATUS = {0: "PSA_OK", 1: "PSA_ERR_INVALID", 2: "PSA_ERR_UNSUPPORTED", 3: "PSA_ERR_WORKSPACE",
+           4: "PSA_ERR_HIP"}
+
+
+def _status_name(s):
+    return _STATUS.get(s, str(s))
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libpsa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libpsa.so is not built: run `python -m paper_2609_37001_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.psa_num_blocks.argtypes = [Grid, i32]
+        L.psa_num_blocks.restype = i32
+        L.psa_workspace_size.argtypes = [i32, i32, Grid, i32]
+        L.psa_workspace_size.restype = sz
+        L.psa_build_blockmap.argtypes = [ctypes.POINTER(Stripe), i32, Grid, i32, vp, vp, vp, vp]
+        L.psa_build_blockmap.restype = ctypes.c_int
+        L.psa_attention_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, i32,
+                                        ctypes.POINTER(Stripe), ctypes.c_float, vp, sz, vp, vp, vp]
+        L.psa_attention_fwd.restype = ctypes.c_int
+        L.psa_dense_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, vp, vp]
+        L.psa_dense_fwd.restype = ctypes.c_int
+        L.psa_status_string.argtypes = [ctypes.c_int]
+        L.psa_status_string.restype = ctypes.c_char_p
+        L.psa_last_error.argtypes = []
+        L.psa_last_error.restype = ctypes.c_char_p
+        _lib = L
+        del i64
+    return _lib
+
+
+def check(status):
+    if status != PSA_OK:
+        raise PsaError(status, lib().psa_last_error().decode())
+    return status
+
+
+def stripes(params):
+    """Host array of psa_stripe_t from a sequence of 6-tuples."""
+    arr = (Stripe * max(1, len(params)))()
+    for i, m in enumerate(params):
+        arr[i] = Stripe(*[int(x) for x in m])
+    return arr
+
+
+def grid_of(frames, height, width, n_text=0):
+    return Grid(int(frames), int(height), int(width), int(n_text))

@@ -1,0 +1,190 @@
+// C ABI of libpsa (declared in include/psa.h): argument validation, workspace layout and
+// kernel dispatch.  All device work lives in psa_kernels.hip.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+
+#include "psa_launch.h"
+
+namespace {
+
+thread_local char g_error[512] = "";
+
+psa_status_t fail(psa_status_t status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_error, sizeof(g_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+psa_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(PSA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Token and block counts of a grid; false if the grid is invalid or too large for int32 indices.
+bool grid_geometry(psa_grid_t grid, int32_t block, psa::Geometry* g) {
+  if (grid.frames < 1 || grid.height < 1 || grid.width < 1 || grid.n_text < 0 || block < 1)
+    return false;
+  const int64_t hw = (int64_t)grid.height * grid.width;
+  const int64_t n_video = hw * grid.frames;
+  const int64_t n = n_video + grid.n_text;
+  if (n + 2 * (int64_t)block >= ((int64_t)1 << 31)) return false;
+  g->hw = (int32_t)hw;
+  g->n_video = (int32_t)n_video;
+  g->n = (int32_t)n;
+  g->n_text = grid.n_text;
+  g->block = block;
+  g->nb = (int32_t)((n + block - 1) / block);
+  return true;
+}
+
+psa_status_t check_params(const psa_stripe_t* params, int32_t n_heads) {
+  if (!params) return fail(PSA_ERR_INVALID, "params is NULL");
+  if (n_heads < 1) return fail(PSA_ERR_INVALID, "n_heads must be >= 1 (got %d)", n_heads);
+  for (int32_t h = 0; h < n_heads; h++) {
+    const psa_stripe_t& m = params[h];
+    if (m.t_w < 1 || m.s_w < 1)
+      return fail(PSA_ERR_INVALID, "head %d: widths must be >= 1 (T_w=%d, S_w=%d)", h, m.t_w, m.s_w);
+    if (m.t_s < 1 || m.s_s < 1)
+      return fail(PSA_ERR_INVALID, "head %d: strides must be >= 1 (T_s=%d, S_s=%d)", h, m.t_s, m.s_s);
+    if (m.t_o > PSA_MAX_OFFSET || m.t_o < -PSA_MAX_OFFSET || m.s_o > PSA_MAX_OFFSET ||
+        m.s_o < -PSA_MAX_OFFSET)
+      return fail(PSA_ERR_INVALID, "head %d: |offset| must be <= %d", h, PSA_MAX_OFFSET);
+  }
+  return PSA_OK;
+}
+
+psa::ParamChunk chunk_of(const psa_stripe_t* params, int32_t head0, int32_t n_heads) {
+  psa::ParamChunk pc;
+  pc.n = std::min(psa::kHeadsPerChunk, n_heads - head0);
+  for (int32_t i = 0; i < psa::kHeadsPerChunk; i++) pc.m[i] = i < pc.n ? params[head0 + i] : params[head0];
+  return pc;
+}
+
+psa_status_t check_attention_shape(int32_t batch, int32_t n_heads, int32_t head_dim,
+                                   int32_t block) {
+  if (batch < 1) return fail(PSA_ERR_INVALID, "batch must be >= 1 (got %d)", batch);
+  if (n_heads < 1) return fail(PSA_ERR_INVALID, "n_heads must be >= 1 (got %d)", n_heads);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(PSA_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", head_dim);
+  if (block != 64 && block != 128)
+    return fail(PSA_ERR_UNSUPPORTED, "block must be 64 or 128 (got %d)", block);
+  return PSA_OK;
+}
+
+int32_t persistent_workgroups() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return 256;
+  return cus;  // one 4-wave workgroup per CU (the tile engine uses 144 KB of LDS)
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t psa_num_blocks(psa_grid_t grid, int32_t block) {
+  psa::Geometry g;
+  return grid_geometry(grid, block, &g) ? g.nb : -1;
+}
+
+size_t psa_workspace_size(int32_t batch, int32_t n_heads, psa_grid_t grid, int32_t block) {
+  psa::Geometry g;
+  if (batch < 1 || n_heads < 1 || !grid_geometry(grid, block, &g)) return 0;
+  return psa::workspace_layout(batch, n_heads, g.nb).total;
+}
+
+psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa_grid_t grid,
+                                int32_t block, uint8_t* blockmap, int32_t* kept_per_row,
+                                int64_t* kept_per_head, hipStream_t stream) {
+  psa::Geometry g;
+  if (!grid_geometry(grid, block, &g))
+    return fail(PSA_ERR_INVALID, "invalid grid (%d x %d x %d + %d text) or block %d", grid.frames,
+                grid.height, grid.width, grid.n_text, block);
+  psa_status_t s = check_params(params, n_heads);
+  if (s != PSA_OK) return s;
+  if ((int64_t)g.nb * g.nb >= ((int64_t)1 << 40))
+    return fail(PSA_ERR_UNSUPPORTED, "block map of %d x %d blocks is too large", g.nb, g.nb);
+  for (int32_t h0 = 0; h0 < n_heads; h0 += psa::kHeadsPerChunk) {
+    const psa::ParamChunk pc = chunk_of(params, h0, n_heads);
+    hipError_t e = psa::launch_blockmap(pc, h0, g, blockmap, kept_per_row, kept_per_head, stream);
+    if (e != hipSuccess) return hip_fail(e, "psa_build_blockmap launch");
+  }
+  return PSA_OK;
+}
+
+psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void* o,
+                               int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
+                               int32_t block, const psa_stripe_t* params, float softmax_scale,
+                               void* workspace, size_t workspace_bytes, float* lse,
+                               int32_t* kept_per_row, hipStream_t stream) {
+  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
+  psa_status_t s = check_attention_shape(batch, n_heads, head_dim, block);
+  if (s != PSA_OK) return s;
+  psa::Geometry g;
+  if (!grid_geometry(grid, block, &g))
+    return fail(PSA_ERR_INVALID, "invalid grid (%d x %d x %d + %d text)", grid.frames, grid.height,
+                grid.width, grid.n_text);
+  s = check_params(params, n_heads);
+  if (s != PSA_OK) return s;
+  if (g.nb > PSA_MAX_BLOCKS)
+    return fail(PSA_ERR_UNSUPPORTED, "%d blocks per sequence exceed %d", g.nb, PSA_MAX_BLOCKS);
+  if ((int64_t)batch * n_heads > PSA_MAX_BATCH_HEADS)
+    return fail(PSA_ERR_UNSUPPORTED, "batch*n_heads = %lld exceeds %d", (long long)batch * n_heads,
+                PSA_MAX_BATCH_HEADS);
+  if ((int64_t)batch * n_heads * g.nb >= ((int64_t)1 << 31))
+    return fail(PSA_ERR_UNSUPPORTED, "too many work items");
+  const psa::WorkspaceLayout wl = psa::workspace_layout(batch, n_heads, g.nb);
+  if (!workspace || workspace_bytes < wl.total)
+    return fail(PSA_ERR_WORKSPACE, "workspace of %zu bytes at %p; %zu bytes required", workspace_bytes,
+                workspace, wl.total);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(PSA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  for (int32_t h0 = 0; h0 < n_heads; h0 += psa::kHeadsPerChunk) {
+    const psa::ParamChunk pc = chunk_of(params, h0, n_heads);
+    hipError_t e = psa::launch_setup(pc, h0, g, workspace, wl, h0 == 0, stream);
+    if (e != hipSuccess) return hip_fail(e, "psa_attention_fwd setup launch");
+  }
+  hipError_t e = psa::launch_schedule(g, batch, n_heads, workspace, wl, kept_per_row, stream);
+  if (e != hipSuccess) return hip_fail(e, "psa_attention_fwd schedule launch");
+  const float c = softmax_scale * 1.4426950408889634f;
+  e = psa::launch_sparse(q, k, v, o, lse, batch, n_heads, head_dim, g, c, workspace, wl,
+                         persistent_workgroups(), stream);
+  if (e != hipSuccess) return hip_fail(e, "psa_attention_fwd kernel launch");
+  return PSA_OK;
+}
+
+psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o, int32_t batch,
+                           int32_t n_heads, int32_t head_dim, int32_t n_tokens, int32_t block,
+                           float softmax_scale, float* lse, hipStream_t stream) {
+  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
+  psa_status_t s = check_attention_shape(batch, n_heads, head_dim, block);
+  if (s != PSA_OK) return s;
+  if (n_tokens < 1 || (int64_t)n_tokens + 2 * block >= ((int64_t)1 << 31))
+    return fail(PSA_ERR_INVALID, "n_tokens must be in [1, 2^31 - 2*block) (got %d)", n_tokens);
+  const int64_t items = (int64_t)batch * n_heads * ((n_tokens + block - 1) / block);
+  if (items + 8 >= ((int64_t)1 << 31)) return fail(PSA_ERR_UNSUPPORTED, "too many work items");
+  const float c = softmax_scale * 1.4426950408889634f;
+  hipError_t e = psa::launch_dense(q, k, v, o, lse, batch, n_heads, head_dim, n_tokens, block, c, stream);
+  if (e != hipSuccess) return hip_fail(e, "psa_dense_fwd kernel launch");
+  return PSA_OK;
+}
+
+const char* psa_status_string(psa_status_t status) {
+  switch (status) {
+    case PSA_OK: return "PSA_OK";
+    case PSA_ERR_INVALID: return "PSA_ERR_INVALID: invalid argument";
+    case PSA_ERR_UNSUPPORTED: return "PSA_ERR_UNSUPPORTED: unsupported shape";
+    case PSA_ERR_WORKSPACE: return "PSA_ERR_WORKSPACE: workspace missing or too small";
+    case PSA_ERR_HIP: return "PSA_ERR_HIP: HIP runtime error";
+  }
+  return "unknown psa_status_t";
+}
+
+const char* psa_last_error(void) { return g_error; }
+
+}  // extern "C"

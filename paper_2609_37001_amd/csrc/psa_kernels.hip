@@ -1,0 +1,687 @@
+// PSA block-sparse attention forward: HIP kernels for gfx950 (CDNA4, MI355X).
+//
+// Kernels
+//   psa_blockmap_kernel / psa_rowcount_kernel  block map and kept counts (Algorithm 1 per block)
+//   psa_setup_kernel                           stripe parameters and block coordinates -> workspace
+//   psa_count_kernel                           kept key blocks of every (batch, head, query block)
+//   psa_schedule_kernel                        load-balanced work order split over 8 XCD queues
+//   psa_sparse_kernel                          persistent block-sparse attention (Algorithm 2)
+//   psa_dense_kernel                           the same tile engine with every block kept
+//
+// Tile engine (one workgroup of 4 wave64s per query block of BLK rows, head dim D):
+//   * wave w = (qi, ki) = (w & 1, w >> 1) owns queries [qi*BLK/2, +BLK/2) of the query block and
+//     keys [ki*BLK/2, +BLK/2) of every key/value block.  Each wave runs its own online softmax
+//     over its key half; the two halves are merged once per work item.  This keeps the LDS
+//     read volume at one K and one V byte per 64 queries, inside the ~128 B/clk/CU LDS budget
+//     at full MFMA rate.
+//   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: K rows come from LDS (A operand), Q^T stays in
+//     registers (B operand).  K rows are read in a permuted order so that each lane's fp32
+//     accumulators hold 8 consecutive keys of every 16-key chunk, which is exactly the B operand
+//     layout of the next product: P^T needs no data movement.
+//   * O^T += V^T P^T: V stays row-major in LDS and the A operand is assembled with the gfx950 LDS
+//     transpose read (ds_read_b64_tr_b16).
+//   * K and V blocks are double-buffered in LDS and filled by direct global->LDS 16-byte loads
+//     (global_load_lds_dwordx4) issued one block ahead; 16-byte chunks are XOR-swizzled per row
+//     so both the K reads and the transposed V reads are bank-conflict free.
+//   * Softmax runs in the exp2 domain with scale*log2(e) folded into one FMA; the running max
+//     is raised lazily (only when a new max exceeds it by more than 2^8), which is exact.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "psa_launch.h"
+
+namespace psa {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+#define PSA_LDS __attribute__((address_space(3)))
+
+// ---------------------------------------------------------------------------------------------
+// Stripe decoder: Algorithm 1 evaluated on block coordinates.
+// ---------------------------------------------------------------------------------------------
+
+// One axis of Algorithm 1: (|delta - offset| mod stride) <= width - 1.
+__device__ __forceinline__ bool axis_keep(int32_t delta, int32_t width, int32_t offset,
+                                          int32_t stride) {
+  const int32_t x = delta - offset;
+  const uint32_t ax = (uint32_t)(x < 0 ? -x : x);
+  return (ax % (uint32_t)stride) < (uint32_t)width;
+}
+
+// Coordinates of block b from its first token: frame t and slot s; t = -1 marks a global block
+// (a block holding at least one appended text token).
+__device__ __forceinline__ int2 block_coord(const Geometry& g, int32_t b) {
+  const int32_t i0 = b * g.block;
+  const int32_t len = min(g.block, g.n - i0);
+  if (g.n_text > 0 && i0 + len > g.n_video) return make_int2(-1, 0);
+  const int32_t t = i0 / g.hw;
+  return make_int2(t, (i0 - t * g.hw) / g.block);
+}
+
+__device__ __forceinline__ bool tile_keep(const psa_stripe_t& m, int2 q, int2 k) {
+  if (q.x < 0 || k.x < 0) return true;
+  return axis_keep(k.x - q.x, m.t_w, m.t_o, m.t_s) && axis_keep(k.y - q.y, m.s_w, m.s_o, m.s_s);
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Block map (psa_build_blockmap).
+// ---------------------------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void psa_blockmap_kernel(ParamChunk pc, int32_t head0,
+                                                           Geometry g, uint8_t* __restrict__ map) {
+  const int32_t hc = blockIdx.y;
+  const int64_t pairs = (int64_t)g.nb * g.nb;
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= pairs) return;
+  const int32_t qb = (int32_t)(p / g.nb), kb = (int32_t)(p - (int64_t)qb * g.nb);
+  const bool keep = tile_keep(pc.m[hc], block_coord(g, qb), block_coord(g, kb));
+  map[(int64_t)(head0 + hc) * pairs + p] = keep ? 1 : 0;
+}
+
+// One workgroup per head: per-row counts and the head total (deterministic, no atomics).
+__global__ __launch_bounds__(256) void psa_rowcount_kernel(ParamChunk pc, int32_t head0,
+                                                           Geometry g,
+                                                           int32_t* __restrict__ kept_per_row,
+                                                           int64_t* __restrict__ kept_per_head) {
+  __shared__ int64_t partial[4];
+  const int32_t hc = blockIdx.x, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const psa_stripe_t m = pc.m[hc];
+  int64_t total = 0;
+  for (int32_t qb = wave; qb < g.nb; qb += 4) {
+    const int2 cq = block_coord(g, qb);
+    int cnt = 0;
+    for (int32_t kb = lane; kb < g.nb; kb += 64) cnt += tile_keep(m, cq, block_coord(g, kb)) ? 1 : 0;
+    cnt = wave_sum(cnt);
+    if (lane == 0 && kept_per_row) kept_per_row[(int64_t)(head0 + hc) * g.nb + qb] = cnt;
+    total += cnt;
+  }
+  if (lane == 0) partial[wave] = total;
+  __syncthreads();
+  if (threadIdx.x == 0 && kept_per_head)
+    kept_per_head[head0 + hc] = partial[0] + partial[1] + partial[2] + partial[3];
+}
+
+hipError_t launch_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& g,
+                           uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
+                           hipStream_t stream) {
+  if (blockmap) {
+    const int64_t pairs = (int64_t)g.nb * g.nb;
+    dim3 grid((unsigned)((pairs + 255) / 256), (unsigned)pc.n);
+    hipLaunchKernelGGL(psa_blockmap_kernel, grid, dim3(256), 0, stream, pc, head0, g, blockmap);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (kept_per_row || kept_per_head) {
+    hipLaunchKernelGGL(psa_rowcount_kernel, dim3(pc.n), dim3(256), 0, stream, pc, head0, g,
+                       kept_per_row, kept_per_head);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Scheduler pre-pass (psa_attention_fwd).
+// ---------------------------------------------------------------------------------------------
+
+WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb) {
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t items = (size_t)batch * n_heads * nb;
+  WorkspaceLayout wl;
+  wl.params = 0;
+  wl.coords = up(wl.params + sizeof(psa_stripe_t) * (size_t)n_heads);
+  wl.counts = up(wl.coords + sizeof(int2) * (size_t)nb);
+  wl.order = up(wl.counts + sizeof(int32_t) * items);
+  wl.queues = up(wl.order + sizeof(int32_t) * items);
+  wl.total = up(wl.queues + sizeof(int32_t) * (2 * kNumQueues + 1));
+  return wl;
+}
+
+// Copies one chunk of stripe parameters into the workspace; the first chunk also writes the
+// block coordinate table.
+__global__ __launch_bounds__(256) void psa_setup_kernel(ParamChunk pc, int32_t head0, Geometry g,
+                                                        psa_stripe_t* __restrict__ params,
+                                                        int2* __restrict__ coords,
+                                                        int32_t write_coords) {
+  const int32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (i < pc.n) params[head0 + i] = pc.m[i];
+  if (write_coords && i < g.nb) coords[i] = block_coord(g, i);
+}
+
+hipError_t launch_setup(const ParamChunk& pc, int32_t head0, const Geometry& g, void* workspace,
+                        const WorkspaceLayout& wl, bool write_coords, hipStream_t stream) {
+  char* ws = (char*)workspace;
+  const int32_t n = write_coords ? max(g.nb, pc.n) : pc.n;
+  hipLaunchKernelGGL(psa_setup_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, pc, head0, g,
+                     (psa_stripe_t*)(ws + wl.params), (int2*)(ws + wl.coords),
+                     (int32_t)(write_coords ? 1 : 0));
+  return hipGetLastError();
+}
+
+// One wave per work item (batch, head, query block): number of kept key blocks.
+__global__ __launch_bounds__(256) void psa_count_kernel(const psa_stripe_t* __restrict__ params,
+                                                        const int2* __restrict__ coords,
+                                                        int32_t* __restrict__ counts,
+                                                        int32_t* __restrict__ kept_per_row,
+                                                        int32_t n_items, int32_t n_heads,
+                                                        int32_t nb) {
+  const int32_t item = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (item >= n_items) return;
+  const int32_t bh = item / nb, qb = item - bh * nb, h = bh % n_heads;
+  const psa_stripe_t m = params[h];
+  const int2 cq = coords[qb];
+  int cnt = 0;
+  for (int32_t kb = lane; kb < nb; kb += 64) cnt += tile_keep(m, cq, coords[kb]) ? 1 : 0;
+  cnt = wave_sum(cnt);
+  if (lane == 0) {
+    counts[item] = cnt;
+    if (kept_per_row && bh < n_heads) kept_per_row[(int64_t)h * nb + qb] = cnt;
+  }
+}
+
+// Work estimate of an item, in tiles: kept key blocks plus a fixed cost for loading Q,
+// decoding the list and the epilogue.
+constexpr int kItemOverhead = 2;
+
+// Single workgroup.  Orders (batch, head) pairs by total work, longest first, keeps query blocks
+// of one head contiguous (so the workgroups of one XCD stream neighbouring K/V blocks through
+// the same L2), and cuts the ordered list into kNumQueues contiguous ranges of equal work.
+__global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __restrict__ counts,
+                                                            int32_t* __restrict__ order,
+                                                            int32_t* __restrict__ queues,
+                                                            int32_t n_bh, int32_t nb) {
+  __shared__ int64_t total[PSA_MAX_BATCH_HEADS];
+  __shared__ int64_t prefix[PSA_MAX_BATCH_HEADS + 1];
+  __shared__ int32_t by_rank[PSA_MAX_BATCH_HEADS];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  for (int32_t bh = wave; bh < n_bh; bh += 16) {
+    int64_t s = 0;
+    for (int32_t qb = lane; qb < nb; qb += 64) s += counts[(int64_t)bh * nb + qb] + kItemOverhead;
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if (lane == 0) total[bh] = s;
+  }
+  __syncthreads();
+  for (int32_t bh = tid; bh < n_bh; bh += 1024) {
+    int32_t r = 0;
+    const int64_t mine = total[bh];
+    for (int32_t j = 0; j < n_bh; j++) r += (total[j] > mine || (total[j] == mine && j < bh)) ? 1 : 0;
+    by_rank[r] = bh;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    prefix[0] = 0;
+    for (int32_t r = 0; r < n_bh; r++) prefix[r + 1] = prefix[r] + total[by_rank[r]];
+  }
+  __syncthreads();
+  const int64_t n_items = (int64_t)n_bh * nb;
+  for (int64_t p = tid; p < n_items; p += 1024) {
+    const int32_t r = (int32_t)(p / nb), qb = (int32_t)(p - (int64_t)r * nb);
+    order[p] = by_rank[r] * nb + qb;
+  }
+  if (tid >= 1 && tid < kNumQueues) {
+    const int64_t target = prefix[n_bh] * tid / kNumQueues;
+    int32_t lo = 0, hi = n_bh;  // largest r with prefix[r] <= target
+    while (lo < hi) {
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (prefix[mid] <= target) lo = mid; else hi = mid - 1;
+    }
+    int32_t boundary = (int32_t)n_items;
+    if (lo < n_bh) {
+      int64_t acc = prefix[lo];
+      const int32_t bh = by_rank[lo];
+      int32_t qb = 0;
+      while (qb < nb && acc < target) acc += counts[(int64_t)bh * nb + qb++] + kItemOverhead;
+      boundary = lo * nb + qb;
+    }
+    queues[tid] = boundary;
+  }
+  if (tid == 0) {
+    queues[0] = 0;
+    queues[kNumQueues] = (int32_t)n_items;
+  }
+  if (tid < kNumQueues) queues[kNumQueues + 1 + tid] = 0;
+}
+
+hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, void* workspace,
+                           const WorkspaceLayout& wl, int32_t* kept_per_row, hipStream_t stream) {
+  char* ws = (char*)workspace;
+  const int32_t n_items = batch * n_heads * g.nb;
+  hipLaunchKernelGGL(psa_count_kernel, dim3((n_items + 3) / 4), dim3(256), 0, stream,
+                     (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
+                     (int32_t*)(ws + wl.counts), kept_per_row, n_items, n_heads, g.nb);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(psa_schedule_kernel, dim3(1), dim3(1024), 0, stream,
+                     (const int32_t*)(ws + wl.counts), (int32_t*)(ws + wl.order),
+                     (int32_t*)(ws + wl.queues), batch * n_heads, g.nb);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------------
+// Tile engine.
+// ---------------------------------------------------------------------------------------------
+
+template <int D, int BLK>
+struct Tile {
+  static constexpr int kWaves = BLK / 32;      // one wave per 32 query rows
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int KT = BLK / 32;          // 32-key row groups of S^T
+  static constexpr int DC = D / 16;            // 16-wide head-dim chunks (Q K^T contraction)
+  static constexpr int DT = D / 32;            // 32-row head-dim groups of O^T
+  static constexpr int KC = BLK / 16;          // 16-key chunks (P V contraction)
+  static constexpr int RB = D * 2;             // LDS bytes per row
+  static constexpr int CPR = D / 8;            // 16-byte chunks per row
+  static constexpr int BYTES = BLK * RB;       // one K or V block in LDS
+  static constexpr int LPW = BYTES / (1024 * kWaves);  // 1 KB DMA slots per wave per tensor
+  static_assert(LPW >= 1 && BYTES % (1024 * kWaves) == 0, "tile shape");
+};
+
+// XOR swizzle of the 16-byte chunks of LDS row `row`.  K reads touch rows
+// {x..x+3, x+8..x+11} per 8 lanes (and {x..x+15} per 16 lanes); transposed V reads touch
+// 4 consecutive rows; both map to distinct banks.
+template <int CPR>
+__device__ __forceinline__ int swz(int row) {
+  int s = ((row & 3) << 1) | ((row >> 3) & 1);
+  if constexpr (CPR == 16) s |= ((row >> 2) & 1) << 3;
+  return s;
+}
+
+// Lane l supplies K row sigma(l & 31) of a 32-row group so that accumulator element i of lane l
+// holds key 16*(i/8) + 8*(l/32) + (i%8).
+__device__ __forceinline__ int key_perm(int r) {
+  const int a = r >> 3, hh = (r >> 2) & 1, b = r & 3;
+  return 16 * (a >> 1) + 8 * hh + 4 * (a & 1) + b;
+}
+
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ void wait_dma_and_sync() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+}
+
+// Direct global->LDS loads of one key/value block.  DMA slot j (1 KB) of the block is loaded by
+// wave j / LPW; its lane l writes LDS bytes [1024 j + 16 l, +16): row (64 j + l) / CPR, physical
+// chunk (64 j + l) % CPR, which holds logical chunk (physical ^ swz(row)).  The loads are issued
+// from inline assembly (SGPR base + 32-bit lane offset, M0 = LDS destination); the compiler does
+// not track them, so every consumer first waits with wait_dma_and_sync().
+template <int D, int BLK>
+struct DmaPlan {
+  using T = Tile<D, BLK>;
+  static constexpr int kRowsPerSlot = 64 / T::CPR;
+  int row[T::LPW];      // row of the block this lane fills in slot i
+  int chunk[T::LPW];    // byte offset of the logical chunk within the row
+  uint32_t lds0;        // LDS byte address of this wave's first slot (stage 0, K)
+
+  __device__ __forceinline__ void init(uint32_t smem_base, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < T::LPW; i++) {
+      const int p = (wave * T::LPW + i) * 64 + lane;
+      row[i] = p / T::CPR;
+      chunk[i] = ((p % T::CPR) ^ swz<T::CPR>(row[i])) << 4;
+    }
+    lds0 = smem_base + (uint32_t)(wave * T::LPW) * 1024u;
+  }
+};
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)(const PSA_LDS void*)p;
+}
+
+__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, const void* base) {
+  // One wait state separates the M0 write from the LDS DMA that reads it.
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(base)
+               : "memory");
+}
+
+// Load key/value block kb into stage `stage`.  Rows past the sequence end are clamped to the last
+// row: their scores are masked to -inf, so the values are never weighted.
+template <int D, int BLK>
+__device__ __forceinline__ void issue_block(const DmaPlan<D, BLK>& plan, const __bf16* kh,
+                                            const __bf16* vh, int kb, int n, int stage) {
+  using T = Tile<D, BLK>;
+  kb = __builtin_amdgcn_readfirstlane(kb);
+  stage = __builtin_amdgcn_readfirstlane(stage);
+  const int last = n - 1 - kb * BLK;           // last valid row of this block
+  const void* kbase = (const void*)(kh + (size_t)kb * BLK * D);
+  const void* vbase = (const void*)(vh + (size_t)kb * BLK * D);
+  const uint32_t lk = plan.lds0 + (uint32_t)stage * (2u * T::BYTES);
+  const uint32_t lv = lk + (uint32_t)T::BYTES;
+#pragma unroll
+  for (int i = 0; i < T::LPW; i++) {
+    const uint32_t voff = (uint32_t)(min(plan.row[i], last) * T::RB + plan.chunk[i]);
+    dma16(__builtin_amdgcn_readfirstlane(lk + i * 1024u), voff, kbase);
+    dma16(__builtin_amdgcn_readfirstlane(lv + i * 1024u), voff, vbase);
+  }
+}
+
+// Per-wave state: 32 query rows (lane l owns row l & 31; lanes l and l^32 split its keys).
+template <int D, int BLK>
+struct WaveState {
+  using T = Tile<D, BLK>;
+  bf16x8 q[T::DC];     // Q^T B operands
+  f32x16 o[T::DT];     // O^T accumulators
+  float m;             // running max, scaled by scale*log2(e)
+  float l;             // running sum over this lane's keys
+};
+
+// One key/value block: S^T = K Q^T, mask (MASK: block reaches past the sequence end), online
+// softmax, O^T += V^T P^T.
+template <int D, int BLK, bool MASK>
+__device__ __forceinline__ void tile_step(WaveState<D, BLK>& st, const uint8_t* sk,
+                                          const uint8_t* sv, int kb, int n, float c, int lane) {
+  using T = Tile<D, BLK>;
+  const int h = lane >> 5;
+  const int krow0 = key_perm(lane & 31);
+  const int ksw = swz<T::CPR>(krow0);   // identical for krow0 + 32 kt
+
+  f32x16 s[T::KT];
+#pragma unroll
+  for (int kt = 0; kt < T::KT; kt++) s[kt] = (f32x16){};
+#pragma unroll
+  for (int cc = 0; cc < T::DC; cc++) {
+#pragma unroll
+    for (int kt = 0; kt < T::KT; kt++) {
+      const bf16x8 a =
+          *(const bf16x8*)(sk + (krow0 + 32 * kt) * T::RB + (((2 * cc + h) ^ ksw) << 4));
+      s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, st.q[cc], s[kt], 0, 0, 0);
+    }
+  }
+
+  // Keys past the end of the sequence: -inf before the softmax (Algorithm 2, padding).
+  if constexpr (MASK) {
+    const int kbase = kb * BLK + 8 * h;
+#pragma unroll
+    for (int kt = 0; kt < T::KT; kt++)
+#pragma unroll
+      for (int i = 0; i < 16; i++)
+        if (kbase + kt * 32 + 16 * (i >> 3) + (i & 7) >= n) s[kt][i] = -__builtin_inff();
+  }
+
+  // Online softmax; the running max moves only when the block max exceeds it by 2^8.
+  float mx = -__builtin_inff();
+#pragma unroll
+  for (int kt = 0; kt < T::KT; kt++)
+#pragma unroll
+    for (int i = 0; i < 16; i++) mx = fmaxf(mx, s[kt][i]);
+  const float ms = pair_max(mx) * c;
+  const bool need = ms - st.m > 8.0f;     // false for -inf - -inf (NaN)
+  if (__builtin_amdgcn_ballot_w64(need)) {
+    const float alpha = need ? __builtin_amdgcn_exp2f(st.m - ms) : 1.0f;
+    st.m = need ? ms : st.m;
+    st.l *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < T::DT; dt++) st.o[dt] *= alpha;
+  }
+  const float base = st.m == -__builtin_inff() ? 0.0f : st.m;
+
+  // P^T: accumulator elements 8*(j&1)..+7 of group j/2 are keys 16j + 8h + 0..7, which is the
+  // B operand of the 16-key chunk j.
+  bf16x8 p[T::KC];
+  float sum[2] = {0.0f, 0.0f};
+#pragma unroll
+  for (int j = 0; j < T::KC; j++) {
+    f32x8 e;
+#pragma unroll
+    for (int x = 0; x < 8; x++) {
+      e[x] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j >> 1][8 * (j & 1) + x], c, -base));
+      sum[x & 1] += e[x];
+    }
+    p[j] = __builtin_convertvector(e, bf16x8);
+  }
+  st.l += sum[0] + sum[1];
+
+  // V^T operand: within each 16-lane group, source lane 4r+c reads V[key0 + r][d0 + 4c .. +3];
+  // the transpose read hands lane i the four keys key0..key0+3 at head-dim d0 + i.
+  const int g = lane >> 4, j16 = lane & 15;
+  const int vkey = 8 * h + (j16 >> 2);
+  const int vsw0 = swz<T::CPR>(vkey), vsw1 = swz<T::CPR>(vkey + 4);   // identical for vkey + 16 j
+#pragma unroll
+  for (int dt = 0; dt < T::DT; dt++) {
+    const int dd = dt * 32 + 16 * (g & 1) + 4 * (j16 & 3);
+    const int lchunk = dd >> 3, inoff = (dd & 7) * 2;
+#pragma unroll
+    for (int j = 0; j < T::KC; j++) {
+      const uint8_t* a0 = sv + (vkey + 16 * j) * T::RB + ((lchunk ^ vsw0) << 4) + inoff;
+      const uint8_t* a1 = sv + (vkey + 16 * j + 4) * T::RB + ((lchunk ^ vsw1) << 4) + inoff;
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a0);
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a1);
+      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p[j], st.o[dt], 0, 0, 0);
+    }
+  }
+}
+
+// One work item: query block qb of one (batch, head).  `list` holds the kept key blocks in
+// ascending order (SPARSE) or is ignored (dense: every block 0..nkv-1).  `smem` holds two stages
+// of (K block, V block).
+template <int D, int BLK, bool SPARSE>
+__device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
+                                             const __bf16* __restrict__ qh,
+                                             const __bf16* __restrict__ kh,
+                                             const __bf16* __restrict__ vh,
+                                             __bf16* __restrict__ oh, float* __restrict__ lseh,
+                                             int n, int qb, int nkv, const uint16_t* list,
+                                             float c, uint8_t* smem) {
+  using T = Tile<D, BLK>;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int h = lane >> 5, r32 = lane & 31;
+  const int row = qb * BLK + wave * 32 + r32;
+
+  WaveState<D, BLK> st;
+  {
+    const bf16x8* src = (const bf16x8*)(qh + (size_t)min(row, n - 1) * D) + h;
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++) st.q[cc] = src[2 * cc];
+  }
+  st.m = -__builtin_inff();
+  st.l = 0.0f;
+#pragma unroll
+  for (int dt = 0; dt < T::DT; dt++) st.o[dt] = (f32x16){};
+
+  // Key/value blocks alternate between the two LDS stages; block it+1 is in flight while block
+  // it is computed.  Only the last block of a sequence can reach past its end, and it is always
+  // the last of an ascending list.
+  auto kv = [&](int i) { return SPARSE ? (int)list[i] : i; };
+  if (nkv > 0) {
+    issue_block<D, BLK>(plan, kh, vh, kv(0), n, 0);
+    wait_dma_and_sync();
+  }
+  for (int it = 0; it < nkv; it++) {
+    const int kb = kv(it);
+    const int stage = it & 1;
+    if (it + 1 < nkv) issue_block<D, BLK>(plan, kh, vh, kv(it + 1), n, stage ^ 1);
+    const uint8_t* sk = smem + stage * (2 * T::BYTES);
+    const uint8_t* sv = sk + T::BYTES;
+    if ((kb + 1) * BLK > n)
+      tile_step<D, BLK, true>(st, sk, sv, kb, n, c, lane);
+    else
+      tile_step<D, BLK, false>(st, sk, sv, kb, n, c, lane);
+    wait_dma_and_sync();
+  }
+
+  // Epilogue: O = O^T / l, rows past the end are not stored.
+  const float lsum = pair_sum(st.l);
+  const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+  if (row < n) {
+    __bf16* dst = oh + (size_t)row * D + 4 * h;
+#pragma unroll
+    for (int dt = 0; dt < T::DT; dt++)
+#pragma unroll
+      for (int a = 0; a < 4; a++) {
+        const f32x4 v = {st.o[dt][4 * a] * inv, st.o[dt][4 * a + 1] * inv,
+                         st.o[dt][4 * a + 2] * inv, st.o[dt][4 * a + 3] * inv};
+        *(bf16x4*)(dst + dt * 32 + 8 * a) = __builtin_convertvector(v, bf16x4);
+      }
+    if (lseh && h == 0)
+      lseh[row] = lsum > 0.0f ? (st.m + __builtin_log2f(lsum)) * 0.69314718055994530942f
+                              : -__builtin_inff();
+  }
+}
+
+// Persistent sparse attention.  Workgroup w starts on queue w % kNumQueues (its XCD under
+// round-robin dispatch) and moves on to the next queue when one runs dry, so every workgroup
+// exits once all queues are exhausted.
+template <int D, int BLK>
+__global__ __launch_bounds__(BLK * 2) void psa_sparse_kernel(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+    __bf16* __restrict__ o, float* __restrict__ lse, const psa_stripe_t* __restrict__ params,
+    const int2* __restrict__ coords, const int32_t* __restrict__ order,
+    int32_t* __restrict__ queues, int32_t n_heads, int32_t n, int32_t nb, float c) {
+  using T = Tile<D, BLK>;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * T::BYTES];
+  __shared__ uint16_t list[PSA_MAX_BLOCKS];
+  __shared__ int32_t misc[8];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  DmaPlan<D, BLK> plan;
+  plan.init(lds_address(smem), __builtin_amdgcn_readfirstlane(wave), lane);
+  int queue = blockIdx.x % kNumQueues, exhausted = 0;
+  while (true) {
+    if (tid == 0) {
+      int32_t item = -1;
+      while (exhausted < kNumQueues) {
+        const int32_t start = queues[queue], len = queues[queue + 1] - start;
+        const int32_t idx = atomicAdd(&queues[kNumQueues + 1 + queue], 1);
+        if (idx < len) {
+          item = order[start + idx];
+          break;
+        }
+        queue = (queue + 1) % kNumQueues;
+        exhausted++;
+      }
+      misc[7] = item;
+    }
+    __syncthreads();
+    const int32_t item = misc[7];
+    if (item < 0) break;
+    const int32_t bh = item / nb, qb = item - bh * nb;
+    const psa_stripe_t m = params[bh % n_heads];
+
+    // In-kernel decode of the kept key blocks of this query block (ascending).
+    const int2 cq = coords[qb];
+    int32_t nkv = 0;
+    for (int32_t base = 0; base < nb; base += T::kThreads) {
+      const int32_t kb = base + tid;
+      const bool keep = kb < nb && tile_keep(m, cq, coords[kb]);
+      const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
+      if (lane == 0) misc[wave] = __builtin_popcountll(mask);
+      __syncthreads();
+      int32_t pos = nkv, total = 0;
+#pragma unroll
+      for (int w = 0; w < T::kWaves; w++) {
+        pos += w < wave ? misc[w] : 0;
+        total += misc[w];
+      }
+      pos += __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                       __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+      if (keep) list[pos] = (uint16_t)kb;
+      nkv += total;
+      __syncthreads();
+    }
+
+    const size_t off = (size_t)bh * n * D;
+    process_item<D, BLK, true>(plan, q + off, k + off, v + off, o + off,
+                               lse ? lse + (size_t)bh * n : nullptr, n, qb, nkv, list, c, smem);
+  }
+}
+
+// Dense attention: one workgroup per (batch, head, query block); consecutive workgroups of one
+// XCD (round-robin dispatch) take consecutive query blocks.
+template <int D, int BLK>
+__global__ __launch_bounds__(BLK * 2) void psa_dense_kernel(const __bf16* __restrict__ q,
+                                                        const __bf16* __restrict__ k,
+                                                        const __bf16* __restrict__ v,
+                                                        __bf16* __restrict__ o,
+                                                        float* __restrict__ lse, int32_t n,
+                                                        int32_t nb, int32_t n_items, float c) {
+  using T = Tile<D, BLK>;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * T::BYTES];
+  const int32_t per_xcd = gridDim.x / kNumQueues;
+  const int32_t item = (blockIdx.x % kNumQueues) * per_xcd + blockIdx.x / kNumQueues;
+  if (item >= n_items) return;
+  const int32_t bh = item / nb, qb = item - bh * nb;
+  const size_t off = (size_t)bh * n * D;
+  DmaPlan<D, BLK> plan;
+  plan.init(lds_address(smem), __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), threadIdx.x & 63);
+  process_item<D, BLK, false>(plan, q + off, k + off, v + off, o + off,
+                              lse ? lse + (size_t)bh * n : nullptr, n, qb, nb, nullptr, c, smem);
+}
+
+template <int D, int BLK>
+static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, void* o,
+                                  float* lse, int32_t n_heads, const Geometry& g, float c,
+                                  void* workspace, const WorkspaceLayout& wl, int32_t n_wg,
+                                  hipStream_t stream) {
+  char* ws = (char*)workspace;
+  hipLaunchKernelGGL((psa_sparse_kernel<D, BLK>), dim3(n_wg), dim3(Tile<D, BLK>::kThreads), 0, stream,
+                     (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
+                     (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
+                     (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues), n_heads, g.n,
+                     g.nb, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse(const void* q, const void* k, const void* v, void* o, float* lse,
+                         int32_t batch, int32_t n_heads, int32_t head_dim, const Geometry& g,
+                         float c, void* workspace, const WorkspaceLayout& wl, int32_t n_wg,
+                         hipStream_t stream) {
+  (void)batch;
+  if (head_dim == 128 && g.block == 128)
+    return launch_sparse_t<128, 128>(q, k, v, o, lse, n_heads, g, c, workspace, wl, n_wg, stream);
+  if (head_dim == 64 && g.block == 64)
+    return launch_sparse_t<64, 64>(q, k, v, o, lse, n_heads, g, c, workspace, wl, n_wg, stream);
+  if (head_dim == 128 && g.block == 64)
+    return launch_sparse_t<128, 64>(q, k, v, o, lse, n_heads, g, c, workspace, wl, n_wg, stream);
+  if (head_dim == 64 && g.block == 128)
+    return launch_sparse_t<64, 128>(q, k, v, o, lse, n_heads, g, c, workspace, wl, n_wg, stream);
+  return hipErrorInvalidValue;
+}
+
+template <int D, int BLK>
+static hipError_t launch_dense_t(const void* q, const void* k, const void* v, void* o, float* lse,
+                                 int32_t n_bh, int32_t n, float c, hipStream_t stream) {
+  const int32_t nb = (n + BLK - 1) / BLK;
+  const int32_t n_items = n_bh * nb;
+  const int32_t per_xcd = (n_items + kNumQueues - 1) / kNumQueues;
+  hipLaunchKernelGGL((psa_dense_kernel<D, BLK>), dim3(per_xcd * kNumQueues), dim3(Tile<D, BLK>::kThreads), 0, stream,
+                     (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse, n, nb,
+                     n_items, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense(const void* q, const void* k, const void* v, void* o, float* lse,
+                        int32_t batch, int32_t n_heads, int32_t head_dim, int32_t n_tokens,
+                        int32_t block, float c, hipStream_t stream) {
+  const int32_t n_bh = batch * n_heads;
+  if (head_dim == 128 && block == 128)
+    return launch_dense_t<128, 128>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+  if (head_dim == 64 && block == 64)
+    return launch_dense_t<64, 64>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+  if (head_dim == 128 && block == 64)
+    return launch_dense_t<128, 64>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+  if (head_dim == 64 && block == 128)
+    return launch_dense_t<64, 128>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace psa

@@ -1,0 +1,66 @@
+// Internal interface between the C ABI (psa_api.hip) and the kernels (psa_kernels.hip).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+#include "psa.h"
+
+namespace psa {
+
+// Number of work queues of the sparse scheduler: one per XCD of an MI355X (8 XCDs of 32 CUs).
+constexpr int kNumQueues = 8;
+
+// Heads whose stripe parameters travel in one kernel-argument block.
+constexpr int kHeadsPerChunk = 64;
+
+struct ParamChunk {
+  int32_t n;                        // heads in this chunk
+  psa_stripe_t m[kHeadsPerChunk];
+};
+
+// Sequence geometry in blocks.
+struct Geometry {
+  int32_t hw;       // tokens per frame, H*W
+  int32_t n_video;  // F*H*W
+  int32_t n;        // n_video + n_text
+  int32_t n_text;
+  int32_t block;
+  int32_t nb;       // ceil(n / block)
+};
+
+// Workspace of psa_attention_fwd (byte offsets, each 256-aligned).
+struct WorkspaceLayout {
+  size_t params;    // psa_stripe_t [n_heads]
+  size_t coords;    // int2 [nb]: (frame, slot) of each block, frame = -1 for a global block
+  size_t counts;    // int32 [batch*n_heads*nb]: kept key blocks per work item
+  size_t order;     // int32 [batch*n_heads*nb]: work items in schedule order
+  size_t queues;    // int32 [2*kNumQueues+1]: queue boundaries then queue counters
+  size_t total;
+};
+
+WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb);
+
+// Launchers; each returns the hipError_t of its launch(es).
+hipError_t launch_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& g,
+                           uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
+                           hipStream_t stream);
+
+hipError_t launch_setup(const ParamChunk& pc, int32_t head0, const Geometry& g, void* workspace,
+                        const WorkspaceLayout& wl, bool write_coords, hipStream_t stream);
+
+hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, void* workspace,
+                           const WorkspaceLayout& wl, int32_t* kept_per_row, hipStream_t stream);
+
+hipError_t launch_sparse(const void* q, const void* k, const void* v, void* o, float* lse,
+                         int32_t batch, int32_t n_heads, int32_t head_dim, const Geometry& g,
+                         float scale_log2, void* workspace, const WorkspaceLayout& wl,
+                         int32_t n_workgroups, hipStream_t stream);
+
+hipError_t launch_dense(const void* q, const void* k, const void* v, void* o, float* lse,
+                        int32_t batch, int32_t n_heads, int32_t head_dim, int32_t n_tokens,
+                        int32_t block, float scale_log2, hipStream_t stream);
+
+}  // namespace psa

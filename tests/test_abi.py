@@ -1,0 +1,100 @@
+"""C ABI of libpsa.so on the CPU: the library loads, exports every call of include/psa.h, and
+rejects invalid arguments with the documented status codes before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_37001_amd import _lib
+import paper_2609_37001_amd as psa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+INF = _lib.STRIDE_INF
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "psa.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const char\*|int32_t|size_t|psa_status_t)\s+(psa_\w+)\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    assert header_functions() == sorted(_lib.EXPORTS)
+
+
+def test_library_exports_every_header_function():
+    L = _lib.lib()
+    for name in header_functions():
+        assert hasattr(L, name), name
+
+
+def test_num_blocks_and_workspace():
+    L = _lib.lib()
+    assert L.psa_num_blocks(_lib.grid_of(21, 45, 80), 128) == 591
+    assert L.psa_num_blocks(_lib.grid_of(33, 45, 80, 256), 128) == 931
+    assert L.psa_num_blocks(_lib.grid_of(4, 16, 16), 64) == 16
+    assert L.psa_num_blocks(_lib.grid_of(2, 3, 4, 3), 5) == 6
+    assert L.psa_num_blocks(_lib.grid_of(0, 3, 4), 5) == -1
+    assert L.psa_num_blocks(_lib.grid_of(2, 3, 4), 0) == -1
+    assert L.psa_num_blocks(_lib.grid_of(2, 3, 4, -1), 4) == -1
+    ws = psa.workspace_size(1, 40, (21, 45, 80), 128)
+    assert ws >= 2 * 4 * 40 * 591 and ws % 256 == 0
+    assert psa.workspace_size(0, 40, (21, 45, 80), 128) == 0
+
+
+def _attn(q=1, k=1, v=1, o=1, batch=1, heads=1, d=128, grid=(2, 8, 8, 0), block=128, params=None,
+          ws=1, wsb=1 << 20, scale=0.1):
+    L = _lib.lib()
+    params = [(1, 0, INF, 1, 0, INF)] * heads if params is None else params
+    vp = lambda x: ctypes.c_void_p(x) if x else None
+    return L.psa_attention_fwd(vp(q), vp(k), vp(v), vp(o), batch, heads, d, _lib.grid_of(*grid), block,
+                               _lib.stripes(params), scale, vp(ws * 256), wsb, None, None, None)
+
+
+def test_attention_validation_codes():
+    assert _attn(q=0) == _lib.PSA_ERR_INVALID
+    assert _attn(o=0) == _lib.PSA_ERR_INVALID
+    assert _attn(batch=0) == _lib.PSA_ERR_INVALID
+    assert _attn(d=96) == _lib.PSA_ERR_UNSUPPORTED
+    assert _attn(block=32) == _lib.PSA_ERR_UNSUPPORTED
+    assert _attn(grid=(0, 8, 8, 0)) == _lib.PSA_ERR_INVALID
+    assert _attn(params=[(0, 0, 1, 1, 0, 1)]) == _lib.PSA_ERR_INVALID
+    assert _attn(params=[(1, 0, 0, 1, 0, 1)]) == _lib.PSA_ERR_INVALID
+    assert _attn(params=[(1, 1 << 25, 1, 1, 0, 1)]) == _lib.PSA_ERR_INVALID
+    assert _attn(ws=0) == _lib.PSA_ERR_WORKSPACE
+    assert _attn(wsb=16) == _lib.PSA_ERR_WORKSPACE
+    assert _attn(grid=(100, 100, 128, 0)) == _lib.PSA_ERR_UNSUPPORTED        # 10000 blocks
+    assert _attn(batch=4097) == _lib.PSA_ERR_UNSUPPORTED
+
+
+def test_error_messages():
+    L = _lib.lib()
+    assert _attn(params=[(1, 0, 0, 1, 0, 1)]) == _lib.PSA_ERR_INVALID
+    assert b"stride" in L.psa_last_error()
+    for s in range(5):
+        assert L.psa_status_string(s).startswith(b"PSA_")
+    with pytest.raises(_lib.PsaError) as e:
+        _lib.check(_attn(d=80))
+    assert e.value.status == _lib.PSA_ERR_UNSUPPORTED
+
+
+def test_dense_validation_codes():
+    L = _lib.lib()
+    vp = ctypes.c_void_p
+    args = lambda n, d, blk, q=256: (vp(q), vp(256), vp(256), vp(256), 1, 1, d, n, blk, 0.1, None, None)
+    assert L.psa_dense_fwd(*args(0, 128, 128)) == _lib.PSA_ERR_INVALID
+    assert L.psa_dense_fwd(*args(100, 48, 128)) == _lib.PSA_ERR_UNSUPPORTED
+    assert L.psa_dense_fwd(*args(100, 64, 16)) == _lib.PSA_ERR_UNSUPPORTED
+    assert L.psa_dense_fwd(*args(100, 64, 64, q=0)) == _lib.PSA_ERR_INVALID
+
+
+def test_blockmap_validation_codes():
+    L = _lib.lib()
+    bad = L.psa_build_blockmap(_lib.stripes([(1, 0, 1, 0, 0, 1)]), 1, _lib.grid_of(2, 2, 2), 1,
+                               None, None, None, None)
+    assert bad == _lib.PSA_ERR_INVALID
+    assert L.psa_build_blockmap(_lib.stripes([(1, 0, 1, 1, 0, 1)]), 0, _lib.grid_of(2, 2, 2), 1,
+                                None, None, None, None) == _lib.PSA_ERR_INVALID
+    assert L.psa_build_blockmap(_lib.stripes([(1, 0, 1, 1, 0, 1)]), 1, _lib.grid_of(2, 2, 0), 1,
+                                None, None, None, None) == _lib.PSA_ERR_INVALID
+    assert L.psa_build_blockmap(None, 1, _lib.grid_of(2, 2, 2), 1, None, None, None, None) == _lib.PSA_ERR_INVALID

@@ -1,0 +1,127 @@
+"""GPU attention parity against the oracle (sampled rows at full size, full tensors when small)."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_37001_amd as psa
+from workloads import get_config
+from workloads.inputs import bf16_round
+
+import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+INF = 0x7FFFFFFF
+
+
+def dev(x):
+    t = gu.torch()
+    return t.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to("cuda:0").bfloat16()
+
+
+def full_compare(q, k, v, keep, block, scale, o, lse):
+    """Every row of a [B, H, N, d] problem against the oracle."""
+    b, h, n, d = q.shape
+    num = den = mx = mlse = 0.0
+    for bi in range(b):
+        for hi in range(h):
+            o_ref, l_ref = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale)
+            og = o[bi, hi].float().cpu().numpy().astype(np.float64)
+            num += ((og - o_ref) ** 2).sum()
+            den += (o_ref ** 2).sum()
+            mx = max(mx, np.abs(og - o_ref).max())
+            lg = lse[bi, hi].cpu().numpy().astype(np.float64)
+            fin = np.isfinite(l_ref)
+            assert (np.isneginf(lg) == ~fin).all()
+            assert (og[~fin] == 0).all()
+            if fin.any():
+                mlse = max(mlse, np.abs(lg[fin] - l_ref[fin]).max())
+    return math.sqrt(num / den), mx, mlse
+
+
+def random_problem(b, h, n, d, seed):
+    rng = np.random.default_rng(seed)
+    return [bf16_round(rng.standard_normal((b, h, n, d)).astype(np.float32)) for _ in range(3)]
+
+
+def test_tiny_config_full():
+    cfg = get_config("tiny")
+    params = gu.params_of("tiny")
+    q, k, v = gu.device_qkv("tiny")
+    o, lse, kept = psa.attention_fwd(q, k, v, gu.grid_of(cfg), cfg.block, params, cfg.scale,
+                                     return_lse=True, return_kept_per_row=True)
+    gu.torch().cuda.synchronize()
+    bmap = gu.oracle_map(cfg, params)
+    assert (kept.cpu().numpy() == oracle.kept_per_row(bmap)).all()
+    qn, kn, vn = (x.float().cpu().numpy() for x in (q, k, v))
+    rel, mx, mlse = full_compare(qn, kn, vn, bmap, cfg.block, cfg.scale, o, lse)
+    print("tiny: rel_l2 %.2e max_abs %.2e lse %.2e" % (rel, mx, mlse))
+    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+
+
+@pytest.mark.parametrize("d,block", [(64, 64), (128, 128), (128, 64), (64, 128)])
+def test_shapes_ragged_text_batch(d, block):
+    """Every (head_dim, block) variant on a ragged sequence with text tokens, batch 2, 5 heads
+    (including an empty-row offset head and a full head)."""
+    f, hh, ww, nt = 3, 10, 13, 37            # N = 427: several blocks and a ragged tail
+    n = f * hh * ww + nt
+    params = [(1, 1, INF, 1, 0, INF), (2, 0, INF, 3, 1, 5), (1, 0, 2, 2, -1, 3), (3, 0, INF, 4, 0, INF),
+              (1, -1, INF, 1, 1, INF)]
+    q, k, v = random_problem(2, len(params), n, d, seed=d + block)
+    keep = oracle.blockmap(params, f, hh, ww, nt, block)
+    o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, nt), block, params, 0.11, return_lse=True)
+    gu.torch().cuda.synchronize()
+    rel, mx, mlse = full_compare(q, k, v, keep, block, 0.11, o, lse)
+    print("d=%d block=%d: rel_l2 %.2e max_abs %.2e lse %.2e" % (d, block, rel, mx, mlse))
+    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+
+
+@pytest.mark.parametrize("d,block", [(64, 64), (128, 128)])
+def test_dense_full(d, block):
+    n = 3 * block + 29
+    q, k, v = random_problem(1, 3, n, d, seed=7)
+    nb = -(-n // block)
+    keep = np.ones((3, nb, nb), np.uint8)
+    o, lse = psa.dense_fwd(dev(q), dev(k), dev(v), block, 0.09, return_lse=True)
+    gu.torch().cuda.synchronize()
+    rel, mx, mlse = full_compare(q, k, v, keep, block, 0.09, o, lse)
+    print("dense d=%d: rel_l2 %.2e max_abs %.2e lse %.2e" % (d, rel, mx, mlse))
+    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+
+
+def test_full_density_sparse_equals_dense_bitwise():
+    f, hh, ww = 4, 16, 24
+    n = f * hh * ww
+    q, k, v = (dev(x) for x in random_problem(1, 3, n, 128, seed=11))
+    params = [(4, 0, INF, 3, 0, INF), (1, 0, 1, 1, 0, 1), (5, 1, 2, 7, -1, 3)]
+    keep = oracle.blockmap(params, f, hh, ww, 0, 128)
+    assert keep.all()
+    o_s, l_s = psa.attention_fwd(q, k, v, (f, hh, ww, 0), 128, params, 0.08, return_lse=True)
+    o_d, l_d = psa.dense_fwd(q, k, v, 128, 0.08, return_lse=True)
+    gu.torch().cuda.synchronize()
+    assert gu.torch().equal(o_s, o_d) and gu.torch().equal(l_s, l_d)
+
+
+def test_deterministic():
+    cfg = get_config("tiny")
+    params = gu.params_of("tiny")
+    q, k, v = gu.device_qkv("tiny")
+    a = psa.attention_fwd(q, k, v, gu.grid_of(cfg), cfg.block, params, cfg.scale)
+    b = psa.attention_fwd(q, k, v, gu.grid_of(cfg), cfg.block, params, cfg.scale)
+    gu.torch().cuda.synchronize()
+    assert gu.torch().equal(a, b)
+
+
+def test_constant_values_and_empty_rows():
+    f, hh, ww = 4, 8, 16                      # HW = 128: one block per frame
+    n = f * hh * ww
+    q, k, _ = random_problem(1, 1, n, 128, seed=5)
+    v = np.ones_like(q)
+    params = [(1, 1, INF, 1, 0, INF)]        # dt = 1 only: the last frame has no keys
+    o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, 0), 128, params, 0.1, return_lse=True)
+    gu.torch().cuda.synchronize()
+    o = o.float().cpu().numpy()[0, 0]
+    lse = lse.cpu().numpy()[0, 0]
+    assert (o[: 3 * 128] == 1.0).all()
+    assert (o[3 * 128:] == 0).all() and np.isneginf(lse[3 * 128:]).all()
