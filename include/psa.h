@@ -57,7 +57,7 @@ extern "C" {
 #define PSA_MAX_OFFSET (1 << 24)
 
 /* Largest number of blocks per sequence accepted by psa_attention_fwd. */
-#define PSA_MAX_BLOCKS 8192
+#define PSA_MAX_BLOCKS 7936
 
 /* Largest batch * n_heads accepted by psa_attention_fwd (scheduler limit). */
 #define PSA_MAX_BATCH_HEADS 4096

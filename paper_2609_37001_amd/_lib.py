@@ -12,7 +12,7 @@ LIB_PATH = os.path.join(PKG, "libpsa.so")
 
 STRIDE_INF = 0x7FFFFFFF
 MAX_OFFSET = 1 << 24
-MAX_BLOCKS = 8192
+MAX_BLOCKS = 7936
 MAX_BATCH_HEADS = 4096
 
 PSA_OK = 0

@@ -79,7 +79,7 @@ int32_t persistent_workgroups() {
   if (hipGetDevice(&dev) != hipSuccess) return 256;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
     return 256;
-  return cus;  // one 4-wave workgroup per CU (the tile engine uses 144 KB of LDS)
+  return 2 * cus;  // two 4-wave workgroups per CU (about 80 KB of LDS each)
 }
 
 }  // namespace

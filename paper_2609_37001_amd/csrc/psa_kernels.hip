@@ -312,32 +312,35 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ void wait_dma_and_sync() {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-}
 
-// Direct global->LDS loads of one key/value block.  DMA slot j (1 KB) of the block is loaded by
+// Direct global->LDS loads of one K or V block.  DMA slot j (1 KB) of the block is loaded by
 // wave j / LPW; its lane l writes LDS bytes [1024 j + 16 l, +16): row (64 j + l) / CPR, physical
 // chunk (64 j + l) % CPR, which holds logical chunk (physical ^ swz(row)).  The loads are issued
 // from inline assembly (SGPR base + 32-bit lane offset, M0 = LDS destination); the compiler does
-// not track them, so every consumer first waits with wait_dma_and_sync().
+// not track them, so every consumer first waits with wait_dma<N>() and a barrier.
 template <int D, int BLK>
 struct DmaPlan {
   using T = Tile<D, BLK>;
-  static constexpr int kRowsPerSlot = 64 / T::CPR;
-  int row[T::LPW];      // row of the block this lane fills in slot i
-  int chunk[T::LPW];    // byte offset of the logical chunk within the row
-  uint32_t lds0;        // LDS byte address of this wave's first slot (stage 0, K)
+  uint32_t off[T::LPW];  // byte offset in the block of the 16 bytes this lane loads in slot i
+  uint32_t lds_k;        // LDS byte address of this wave's first slot in the K buffer
+  uint32_t lds_v;        // same in the V buffer
+  int wave, lane;
 
-  __device__ __forceinline__ void init(uint32_t smem_base, int wave, int lane) {
+  __device__ __forceinline__ void init(uint32_t k_base, uint32_t v_base, int wave_, int lane_) {
+    wave = wave_;
+    lane = lane_;
 #pragma unroll
-    for (int i = 0; i < T::LPW; i++) {
-      const int p = (wave * T::LPW + i) * 64 + lane;
-      row[i] = p / T::CPR;
-      chunk[i] = ((p % T::CPR) ^ swz<T::CPR>(row[i])) << 4;
-    }
-    lds0 = smem_base + (uint32_t)(wave * T::LPW) * 1024u;
+    for (int i = 0; i < T::LPW; i++) off[i] = offset(i, BLK);
+    lds_k = k_base + (uint32_t)(wave * T::LPW) * 1024u;
+    lds_v = v_base + (uint32_t)(wave * T::LPW) * 1024u;
+  }
+
+  // Offset of slot i with rows at or past `rows` clamped to row rows - 1.
+  __device__ __forceinline__ uint32_t offset(int i, int rows) const {
+    const int p = (wave * T::LPW + i) * 64 + lane;
+    const int row = p / T::CPR;
+    const int chunk = (p % T::CPR) ^ swz<T::CPR>(row);
+    return (uint32_t)(min(row, rows - 1) * T::RB + chunk * 16);
   }
 };
 
@@ -353,24 +356,29 @@ __device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, const vo
                : "memory");
 }
 
-// Load key/value block kb into stage `stage`.  Rows past the sequence end are clamped to the last
-// row: their scores are masked to -inf, so the values are never weighted.
+// Wait until at most N of this wave's DMA loads are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_dma() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Load rows of block kb of one tensor (K or V) into its LDS buffer.  Rows past the sequence end
+// are clamped to the last row: their scores are masked to -inf, so they are never weighted.
 template <int D, int BLK>
-__device__ __forceinline__ void issue_block(const DmaPlan<D, BLK>& plan, const __bf16* kh,
-                                            const __bf16* vh, int kb, int n, int stage) {
+__device__ __forceinline__ void issue_block(const DmaPlan<D, BLK>& plan, const __bf16* xh,
+                                            uint32_t lds, int kb, int n) {
   using T = Tile<D, BLK>;
   kb = __builtin_amdgcn_readfirstlane(kb);
-  stage = __builtin_amdgcn_readfirstlane(stage);
-  const int last = n - 1 - kb * BLK;           // last valid row of this block
-  const void* kbase = (const void*)(kh + (size_t)kb * BLK * D);
-  const void* vbase = (const void*)(vh + (size_t)kb * BLK * D);
-  const uint32_t lk = plan.lds0 + (uint32_t)stage * (2u * T::BYTES);
-  const uint32_t lv = lk + (uint32_t)T::BYTES;
+  const int rows = n - kb * BLK;
+  const void* base = (const void*)(xh + (size_t)kb * BLK * D);
+  if (rows >= BLK) {
 #pragma unroll
-  for (int i = 0; i < T::LPW; i++) {
-    const uint32_t voff = (uint32_t)(min(plan.row[i], last) * T::RB + plan.chunk[i]);
-    dma16(__builtin_amdgcn_readfirstlane(lk + i * 1024u), voff, kbase);
-    dma16(__builtin_amdgcn_readfirstlane(lv + i * 1024u), voff, vbase);
+    for (int i = 0; i < T::LPW; i++)
+      dma16(__builtin_amdgcn_readfirstlane(lds + i * 1024u), plan.off[i], base);
+  } else {
+#pragma unroll
+    for (int i = 0; i < T::LPW; i++)
+      dma16(__builtin_amdgcn_readfirstlane(lds + i * 1024u), plan.offset(i, rows), base);
   }
 }
 
@@ -384,48 +392,72 @@ struct WaveState {
   float l;             // running sum over this lane's keys
 };
 
-// One key/value block: S^T = K Q^T, mask (MASK: block reaches past the sequence end), online
-// softmax, O^T += V^T P^T.
-template <int D, int BLK, bool MASK>
-__device__ __forceinline__ void tile_step(WaveState<D, BLK>& st, const uint8_t* sk,
-                                          const uint8_t* sv, int kb, int n, float c, int lane) {
-  using T = Tile<D, BLK>;
-  const int h = lane >> 5;
-  const int krow0 = key_perm(lane & 31);
-  const int ksw = swz<T::CPR>(krow0);   // identical for krow0 + 32 kt
+// Each key/value block is processed in two halves of HK = BLK/2 keys (S^T: HK/32 groups of 32 keys
+// per wave); every half updates the online-softmax statistics on its own.
+template <int D, int BLK>
+struct Half {
+  static constexpr int HK = BLK / 2;          // keys per half
+  static constexpr int KT = HK / 32;          // 32-key groups of S^T per half
+  static constexpr int KC = HK / 16;          // 16-key chunks per half
+};
 
-  f32x16 s[T::KT];
+// S^T = K Q^T for keys [k0, k0 + HK) of the block (K rows from LDS).
+template <int D, int BLK>
+__device__ __forceinline__ void qk_half(const WaveState<D, BLK>& st,
+                                        f32x16 (&s)[Half<D, BLK>::KT], const uint8_t* sk, int k0,
+                                        int lane) {
+  using T = Tile<D, BLK>;
+  using H = Half<D, BLK>;
+  const int h = lane >> 5;
+  const int krow0 = k0 + key_perm(lane & 31);
+  const int ksw = swz<T::CPR>(krow0);   // identical for krow0 + 32 kt
 #pragma unroll
-  for (int kt = 0; kt < T::KT; kt++) s[kt] = (f32x16){};
+  for (int kt = 0; kt < H::KT; kt++) s[kt] = (f32x16){};
 #pragma unroll
   for (int cc = 0; cc < T::DC; cc++) {
 #pragma unroll
-    for (int kt = 0; kt < T::KT; kt++) {
+    for (int kt = 0; kt < H::KT; kt++) {
       const bf16x8 a =
           *(const bf16x8*)(sk + (krow0 + 32 * kt) * T::RB + (((2 * cc + h) ^ ksw) << 4));
       s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, st.q[cc], s[kt], 0, 0, 0);
     }
   }
+}
 
-  // Keys past the end of the sequence: -inf before the softmax (Algorithm 2, padding).
-  if constexpr (MASK) {
-    const int kbase = kb * BLK + 8 * h;
+// Mask (tail: the block reaches past the sequence end), online-softmax statistics, P^T chunk by
+// chunk and O^T += V^T P^T, for keys [k0, k0 + HK) of block kb.
+//  * The running max moves only when the new max exceeds it by 2^8, so P <= 2^8 (exact).
+//  * Accumulator elements 8*(j&1)..+7 of S^T group j/2 are keys 16j + 8h + 0..7: the B operand
+//    of 16-key chunk j.
+//  * V^T operand: within each 16-lane group, source lane 4r+c reads V[key0 + r][d0 + 4c .. +3];
+//    the transpose read hands lane i the four keys key0..key0+3 at head-dim d0 + i.
+template <int D, int BLK>
+__device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
+                                                f32x16 (&s)[Half<D, BLK>::KT], const uint8_t* sv,
+                                                int kb, int k0, int n, float c, bool tail,
+                                                int lane) {
+  using T = Tile<D, BLK>;
+  using H = Half<D, BLK>;
+  const int h = lane >> 5, g = lane >> 4, j16 = lane & 15;
+  if (tail) {
+    asm volatile("" ::: "memory");        // keep the mask a branch taken once per item
+    const int kbase = kb * BLK + k0 + 8 * h;
 #pragma unroll
-    for (int kt = 0; kt < T::KT; kt++)
+    for (int kt = 0; kt < H::KT; kt++)
 #pragma unroll
       for (int i = 0; i < 16; i++)
         if (kbase + kt * 32 + 16 * (i >> 3) + (i & 7) >= n) s[kt][i] = -__builtin_inff();
   }
 
-  // Online softmax; the running max moves only when the block max exceeds it by 2^8.
   float mx = -__builtin_inff();
 #pragma unroll
-  for (int kt = 0; kt < T::KT; kt++)
+  for (int kt = 0; kt < H::KT; kt++)
 #pragma unroll
     for (int i = 0; i < 16; i++) mx = fmaxf(mx, s[kt][i]);
   const float ms = pair_max(mx) * c;
   const bool need = ms - st.m > 8.0f;     // false for -inf - -inf (NaN)
   if (__builtin_amdgcn_ballot_w64(need)) {
+    asm volatile("" ::: "memory");        // keep this rare path a branch
     const float alpha = need ? __builtin_amdgcn_exp2f(st.m - ms) : 1.0f;
     st.m = need ? ms : st.m;
     st.l *= alpha;
@@ -434,46 +466,61 @@ __device__ __forceinline__ void tile_step(WaveState<D, BLK>& st, const uint8_t* 
   }
   const float base = st.m == -__builtin_inff() ? 0.0f : st.m;
 
-  // P^T: accumulator elements 8*(j&1)..+7 of group j/2 are keys 16j + 8h + 0..7, which is the
-  // B operand of the 16-key chunk j.
-  bf16x8 p[T::KC];
+  const int vkey = k0 + 8 * h + (j16 >> 2);
+  const int vsw0 = swz<T::CPR>(vkey), vsw1 = swz<T::CPR>(vkey + 4);   // identical for vkey + 16 j
   float sum[2] = {0.0f, 0.0f};
 #pragma unroll
-  for (int j = 0; j < T::KC; j++) {
+  for (int j = 0; j < H::KC; j++) {
     f32x8 e;
 #pragma unroll
     for (int x = 0; x < 8; x++) {
       e[x] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j >> 1][8 * (j & 1) + x], c, -base));
       sum[x & 1] += e[x];
     }
-    p[j] = __builtin_convertvector(e, bf16x8);
-  }
-  st.l += sum[0] + sum[1];
-
-  // V^T operand: within each 16-lane group, source lane 4r+c reads V[key0 + r][d0 + 4c .. +3];
-  // the transpose read hands lane i the four keys key0..key0+3 at head-dim d0 + i.
-  const int g = lane >> 4, j16 = lane & 15;
-  const int vkey = 8 * h + (j16 >> 2);
-  const int vsw0 = swz<T::CPR>(vkey), vsw1 = swz<T::CPR>(vkey + 4);   // identical for vkey + 16 j
+    const bf16x8 p = __builtin_convertvector(e, bf16x8);
 #pragma unroll
-  for (int dt = 0; dt < T::DT; dt++) {
-    const int dd = dt * 32 + 16 * (g & 1) + 4 * (j16 & 3);
-    const int lchunk = dd >> 3, inoff = (dd & 7) * 2;
-#pragma unroll
-    for (int j = 0; j < T::KC; j++) {
+    for (int dt = 0; dt < T::DT; dt++) {
+      const int dd = dt * 32 + 16 * (g & 1) + 4 * (j16 & 3);
+      const int lchunk = dd >> 3, inoff = (dd & 7) * 2;
       const uint8_t* a0 = sv + (vkey + 16 * j) * T::RB + ((lchunk ^ vsw0) << 4) + inoff;
       const uint8_t* a1 = sv + (vkey + 16 * j + 4) * T::RB + ((lchunk ^ vsw1) << 4) + inoff;
       const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a0);
       const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a1);
       const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p[j], st.o[dt], 0, 0, 0);
+      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p, st.o[dt], 0, 0, 0);
     }
   }
+  st.l += sum[0] + sum[1];
+}
+
+// One key/value block with a single K and a single V buffer per workgroup:
+//   QK(lo) | wait V(i), barrier | softmax+PV(lo), QK(hi) | barrier, load K(i+1) |
+//   softmax+PV(hi) | wait K(i+1), barrier, load V(i+1)
+// K(i+1) streams in during the second half of block i, V(i+1) during QK(lo) of block i+1; the
+// other workgroup on the CU covers the rest of the load latency.
+template <int D, int BLK>
+__device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<D, BLK>& plan,
+                                           const __bf16* kh, const __bf16* vh, int kb, int kb_next,
+                                           int n, float c, const uint8_t* sk, const uint8_t* sv,
+                                           int lane) {
+  const bool tail = (kb + 1) * BLK > n;
+  using H = Half<D, BLK>;
+  f32x16 s[H::KT];
+  qk_half<D, BLK>(st, s, sk, 0, lane);
+  wait_dma<0>();
+  __syncthreads();
+  softmax_pv_half<D, BLK>(st, s, sv, kb, 0, n, c, tail, lane);
+  qk_half<D, BLK>(st, s, sk, H::HK, lane);
+  __syncthreads();
+  if (kb_next >= 0) issue_block<D, BLK>(plan, kh, plan.lds_k, kb_next, n);
+  softmax_pv_half<D, BLK>(st, s, sv, kb, H::HK, n, c, tail, lane);
+  wait_dma<0>();
+  __syncthreads();
+  if (kb_next >= 0) issue_block<D, BLK>(plan, vh, plan.lds_v, kb_next, n);
 }
 
 // One work item: query block qb of one (batch, head).  `list` holds the kept key blocks in
-// ascending order (SPARSE) or is ignored (dense: every block 0..nkv-1).  `smem` holds two stages
-// of (K block, V block).
+// ascending order (SPARSE) or is ignored (dense: every block 0..nkv-1).
 template <int D, int BLK, bool SPARSE>
 __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
                                              const __bf16* __restrict__ qh,
@@ -481,7 +528,7 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
                                              const __bf16* __restrict__ vh,
                                              __bf16* __restrict__ oh, float* __restrict__ lseh,
                                              int n, int qb, int nkv, const uint16_t* list,
-                                             float c, uint8_t* smem) {
+                                             float c, const uint8_t* sk, const uint8_t* sv) {
   using T = Tile<D, BLK>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, r32 = lane & 31;
@@ -498,25 +545,19 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
 #pragma unroll
   for (int dt = 0; dt < T::DT; dt++) st.o[dt] = (f32x16){};
 
-  // Key/value blocks alternate between the two LDS stages; block it+1 is in flight while block
-  // it is computed.  Only the last block of a sequence can reach past its end, and it is always
-  // the last of an ascending list.
+  // Only the last block of a sequence can reach past its end, and it is always the last of an
+  // ascending list.
   auto kv = [&](int i) { return SPARSE ? (int)list[i] : i; };
   if (nkv > 0) {
-    issue_block<D, BLK>(plan, kh, vh, kv(0), n, 0);
-    wait_dma_and_sync();
+    issue_block<D, BLK>(plan, kh, plan.lds_k, kv(0), n);
+    issue_block<D, BLK>(plan, vh, plan.lds_v, kv(0), n);
+    wait_dma<T::LPW>();
+    __syncthreads();
   }
   for (int it = 0; it < nkv; it++) {
     const int kb = kv(it);
-    const int stage = it & 1;
-    if (it + 1 < nkv) issue_block<D, BLK>(plan, kh, vh, kv(it + 1), n, stage ^ 1);
-    const uint8_t* sk = smem + stage * (2 * T::BYTES);
-    const uint8_t* sv = sk + T::BYTES;
-    if ((kb + 1) * BLK > n)
-      tile_step<D, BLK, true>(st, sk, sv, kb, n, c, lane);
-    else
-      tile_step<D, BLK, false>(st, sk, sv, kb, n, c, lane);
-    wait_dma_and_sync();
+    const int kb_next = it + 1 < nkv ? kv(it + 1) : -1;
+    block_step<D, BLK>(st, plan, kh, vh, kb, kb_next, n, c, sk, sv, lane);
   }
 
   // Epilogue: O = O^T / l, rows past the end are not stored.
@@ -538,23 +579,24 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
   }
 }
 
-// Persistent sparse attention.  Workgroup w starts on queue w % kNumQueues (its XCD under
+// Persistent sparse attention (two 4-wave workgroups per CU).  Workgroup w starts on queue w % kNumQueues (its XCD under
 // round-robin dispatch) and moves on to the next queue when one runs dry, so every workgroup
 // exits once all queues are exhausted.
 template <int D, int BLK>
-__global__ __launch_bounds__(BLK * 2) void psa_sparse_kernel(
+__global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void psa_sparse_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     __bf16* __restrict__ o, float* __restrict__ lse, const psa_stripe_t* __restrict__ params,
     const int2* __restrict__ coords, const int32_t* __restrict__ order,
     int32_t* __restrict__ queues, int32_t n_heads, int32_t n, int32_t nb, float c) {
   using T = Tile<D, BLK>;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * T::BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sk[T::BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sv[T::BYTES];
   __shared__ uint16_t list[PSA_MAX_BLOCKS];
   __shared__ int32_t misc[8];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   DmaPlan<D, BLK> plan;
-  plan.init(lds_address(smem), __builtin_amdgcn_readfirstlane(wave), lane);
+  plan.init(lds_address(sk), lds_address(sv), __builtin_amdgcn_readfirstlane(wave), lane);
   int queue = blockIdx.x % kNumQueues, exhausted = 0;
   while (true) {
     if (tid == 0) {
@@ -601,30 +643,32 @@ __global__ __launch_bounds__(BLK * 2) void psa_sparse_kernel(
 
     const size_t off = (size_t)bh * n * D;
     process_item<D, BLK, true>(plan, q + off, k + off, v + off, o + off,
-                               lse ? lse + (size_t)bh * n : nullptr, n, qb, nkv, list, c, smem);
+                               lse ? lse + (size_t)bh * n : nullptr, n, qb, nkv, list, c, sk, sv);
   }
 }
 
 // Dense attention: one workgroup per (batch, head, query block); consecutive workgroups of one
 // XCD (round-robin dispatch) take consecutive query blocks.
 template <int D, int BLK>
-__global__ __launch_bounds__(BLK * 2) void psa_dense_kernel(const __bf16* __restrict__ q,
+__global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void psa_dense_kernel(const __bf16* __restrict__ q,
                                                         const __bf16* __restrict__ k,
                                                         const __bf16* __restrict__ v,
                                                         __bf16* __restrict__ o,
                                                         float* __restrict__ lse, int32_t n,
                                                         int32_t nb, int32_t n_items, float c) {
   using T = Tile<D, BLK>;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * T::BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sk[T::BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sv[T::BYTES];
   const int32_t per_xcd = gridDim.x / kNumQueues;
   const int32_t item = (blockIdx.x % kNumQueues) * per_xcd + blockIdx.x / kNumQueues;
   if (item >= n_items) return;
   const int32_t bh = item / nb, qb = item - bh * nb;
   const size_t off = (size_t)bh * n * D;
   DmaPlan<D, BLK> plan;
-  plan.init(lds_address(smem), __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), threadIdx.x & 63);
+  plan.init(lds_address(sk), lds_address(sv), __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
+            threadIdx.x & 63);
   process_item<D, BLK, false>(plan, q + off, k + off, v + off, o + off,
-                              lse ? lse + (size_t)bh * n : nullptr, n, qb, nb, nullptr, c, smem);
+                              lse ? lse + (size_t)bh * n : nullptr, n, qb, nb, nullptr, c, sk, sv);
 }
 
 template <int D, int BLK>
