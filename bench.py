@@ -49,6 +49,8 @@ def parse():
     p.add_argument("--no-dense", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--copy-mb", type=int, default=0,
+                   help="run one plain device copy of this many MiB first (counter calibration)")
     return p.parse_args()
 
 
@@ -136,6 +138,13 @@ def main():
     q, k, v = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to("cuda:0")
                for x in make_qkv(cfg, workers=16))
     log("inputs ready in %.1f s" % (time.perf_counter() - t0))
+    if args.copy_mb:
+        src = torch.ones(args.copy_mb << 18, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: %d MiB read, %d MiB written" % (args.copy_mb, args.copy_mb))
+        del src, dst
     o = torch.empty_like(q)
     ws = psa.Workspace(cfg.batch, cfg.heads, grid, cfg.block, q.device)
     flops, density = computed_flops(psa, cfg, params, torch)

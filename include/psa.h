@@ -60,7 +60,7 @@ extern "C" {
 #define PSA_MAX_BLOCKS 7936
 
 /* Largest batch * n_heads accepted by psa_attention_fwd (scheduler limit). */
-#define PSA_MAX_BATCH_HEADS 4096
+#define PSA_MAX_BATCH_HEADS 1024
 
 /* M(T_w, T_o, T_s, S_w, S_o, S_s) of one head (Sec. 3.2).  Widths and strides must be >= 1. */
 typedef struct {

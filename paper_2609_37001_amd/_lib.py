@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(PKG, "libpsa.so")
 STRIDE_INF = 0x7FFFFFFF
 MAX_OFFSET = 1 << 24
 MAX_BLOCKS = 7936
-MAX_BATCH_HEADS = 4096
+MAX_BATCH_HEADS = 1024
 
 PSA_OK = 0
 PSA_ERR_INVALID = 1

@@ -192,17 +192,22 @@ __global__ __launch_bounds__(256) void psa_count_kernel(const psa_stripe_t* __re
 // decoding the list and the epilogue.
 constexpr int kItemOverhead = 2;
 
-// Single workgroup.  Orders (batch, head) pairs by total work, longest first, keeps query blocks
-// of one head contiguous (so the workgroups of one XCD stream neighbouring K/V blocks through
-// the same L2), and cuts the ordered list into kNumQueues contiguous ranges of equal work.
+// Single workgroup.  Orders the (batch, head) pairs by total work, longest first, and cuts every
+// head's query blocks into kNumQueues contiguous ranges of equal work; queue x (the XCD of the
+// workgroups that start on it) lists range x of every head in that order.  All XCDs therefore
+// sweep the heads together -- the K/V of the one or two heads in flight stay in the memory-side
+// cache -- and the workgroups of one XCD stream neighbouring key blocks through its L2.
 __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __restrict__ counts,
                                                             int32_t* __restrict__ order,
                                                             int32_t* __restrict__ queues,
                                                             int32_t n_bh, int32_t nb) {
   __shared__ int64_t total[PSA_MAX_BATCH_HEADS];
-  __shared__ int64_t prefix[PSA_MAX_BATCH_HEADS + 1];
   __shared__ int32_t by_rank[PSA_MAX_BATCH_HEADS];
+  __shared__ uint16_t bounds[PSA_MAX_BATCH_HEADS][kNumQueues + 1];
+  __shared__ int32_t qoff[PSA_MAX_BATCH_HEADS][kNumQueues];
+  __shared__ int32_t qstart[kNumQueues + 1];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+
   for (int32_t bh = wave; bh < n_bh; bh += 16) {
     int64_t s = 0;
     for (int32_t qb = lane; qb < nb; qb += 64) s += counts[(int64_t)bh * nb + qb] + kItemOverhead;
@@ -217,37 +222,64 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
     by_rank[r] = bh;
   }
   __syncthreads();
-  if (tid == 0) {
-    prefix[0] = 0;
-    for (int32_t r = 0; r < n_bh; r++) prefix[r + 1] = prefix[r] + total[by_rank[r]];
+
+  // Equal-work ranges of each head: bounds[r][x] = first query block of range x.
+  for (int32_t r = wave; r < n_bh; r += 16) {
+    const int32_t bh = by_rank[r];
+    const int64_t head_total = total[bh];
+    int64_t base = 0;
+    int32_t next = 1;                       // next boundary to place
+    if (lane == 0) bounds[r][0] = 0;
+    for (int32_t q0 = 0; q0 < nb && next < kNumQueues; q0 += 64) {
+      const int32_t qb = q0 + lane;
+      int64_t w = qb < nb ? counts[(int64_t)bh * nb + qb] + kItemOverhead : 0;
+      int64_t incl = w;                     // inclusive prefix over the wave
+      for (int off = 1; off < 64; off <<= 1) {
+        const int64_t t = __shfl_up(incl, off);
+        if (lane >= off) incl += t;
+      }
+      const int64_t excl = base + incl - w;
+      // range x starts at the first block whose preceding work reaches x/Q of the head
+      while (next < kNumQueues) {
+        const int64_t target = head_total * next / kNumQueues;
+        const uint64_t hit = __builtin_amdgcn_ballot_w64(qb < nb && excl >= target);
+        if (!hit) break;
+        const int32_t first = q0 + __builtin_ctzll(hit);
+        if (lane == 0) bounds[r][next] = (uint16_t)first;
+        next++;
+      }
+      base += __shfl(incl, 63);
+    }
+    for (; next < kNumQueues; next++)
+      if (lane == 0) bounds[r][next] = (uint16_t)nb;
+    if (lane == 0) bounds[r][kNumQueues] = (uint16_t)nb;
   }
   __syncthreads();
-  const int64_t n_items = (int64_t)n_bh * nb;
-  for (int64_t p = tid; p < n_items; p += 1024) {
-    const int32_t r = (int32_t)(p / nb), qb = (int32_t)(p - (int64_t)r * nb);
-    order[p] = by_rank[r] * nb + qb;
-  }
-  if (tid >= 1 && tid < kNumQueues) {
-    const int64_t target = prefix[n_bh] * tid / kNumQueues;
-    int32_t lo = 0, hi = n_bh;  // largest r with prefix[r] <= target
-    while (lo < hi) {
-      const int32_t mid = (lo + hi + 1) >> 1;
-      if (prefix[mid] <= target) lo = mid; else hi = mid - 1;
+
+  // Offsets of each head's range inside its queue, and the queue starts.
+  if (tid < kNumQueues) {
+    int32_t acc = 0;
+    for (int32_t r = 0; r < n_bh; r++) {
+      qoff[r][tid] = acc;
+      acc += bounds[r][tid + 1] - bounds[r][tid];
     }
-    int32_t boundary = (int32_t)n_items;
-    if (lo < n_bh) {
-      int64_t acc = prefix[lo];
-      const int32_t bh = by_rank[lo];
-      int32_t qb = 0;
-      while (qb < nb && acc < target) acc += counts[(int64_t)bh * nb + qb++] + kItemOverhead;
-      boundary = lo * nb + qb;
-    }
-    queues[tid] = boundary;
+    qstart[tid + 1] = acc;                  // length, turned into a start below
   }
+  __syncthreads();
   if (tid == 0) {
-    queues[0] = 0;
-    queues[kNumQueues] = (int32_t)n_items;
+    qstart[0] = 0;
+    for (int x = 0; x < kNumQueues; x++) qstart[x + 1] += qstart[x];
   }
+  __syncthreads();
+
+  for (int32_t pair = tid; pair < n_bh * kNumQueues; pair += 1024) {
+    const int32_t r = pair / kNumQueues, x = pair - r * kNumQueues;
+    const int32_t item0 = by_rank[r] * nb;
+    int32_t* dst = order + qstart[x] + qoff[r][x];
+    const int32_t lo = bounds[r][x], hi = bounds[r][x + 1];
+    for (int32_t qb = lo; qb < hi; qb++) dst[qb - lo] = item0 + qb;
+  }
+  if (tid <= kNumQueues) queues[tid] = qstart[tid];
   if (tid < kNumQueues) queues[kNumQueues + 1 + tid] = 0;
 }
 
@@ -285,14 +317,18 @@ struct Tile {
   static_assert(LPW >= 1 && BYTES % (1024 * kWaves) == 0, "tile shape");
 };
 
-// XOR swizzle of the 16-byte chunks of LDS row `row`.  K reads touch rows
-// {x..x+3, x+8..x+11} per 8 lanes (and {x..x+15} per 16 lanes); transposed V reads touch
-// 4 consecutive rows; both map to distinct banks.
+// XOR swizzle of the 16-byte chunks of LDS row `row` (D = 128: 16 chunks per row).  K reads
+// touch the 16 rows {x..x+15} (8 lanes per cycle: rows {x..x+3, x+8..x+11}) at one logical
+// chunk; transposed V reads touch 4 consecutive rows r0..r0+3 at 4 consecutive chunks (16 lanes
+// per cycle: 2 chunks).  Within a quad of rows, bits (1,2) and bits (2,3) of the swizzle are
+// both all distinct; row bits 2 and 3 flip bits 1 and 0.  Every one of these access groups then
+// hits distinct banks whether the LDS serves 128 or 256 bytes per clock.
 template <int CPR>
 __device__ __forceinline__ int swz(int row) {
-  int s = ((row & 3) << 1) | ((row >> 3) & 1);
-  if constexpr (CPR == 16) s |= ((row >> 2) & 1) << 3;
-  return s;
+  const int i = row & 3;
+  const int s = (((i >> 1) << 3) | ((i & 1) << 2) | ((i >> 1) << 1)) ^ (((row >> 2) & 1) << 1) ^
+                ((row >> 3) & 1);
+  return s & (CPR - 1);
 }
 
 // Lane l supplies K row sigma(l & 31) of a 32-row group so that accumulator element i of lane l
@@ -539,6 +575,11 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
     const bf16x8* src = (const bf16x8*)(qh + (size_t)min(row, n - 1) * D) + h;
 #pragma unroll
     for (int cc = 0; cc < T::DC; cc++) st.q[cc] = src[2 * cc];
+    // Consume the Q registers here: the compiler then waits for these loads once, before any
+    // K/V DMA is issued, instead of inside the block loop where the hardware counter also
+    // counts the in-flight DMA.
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++) asm volatile("" ::"v"(st.q[cc]));
   }
   st.m = -__builtin_inff();
   st.l = 0.0f;

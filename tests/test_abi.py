@@ -64,7 +64,7 @@ def test_attention_validation_codes():
     assert _attn(ws=0) == _lib.PSA_ERR_WORKSPACE
     assert _attn(wsb=16) == _lib.PSA_ERR_WORKSPACE
     assert _attn(grid=(100, 100, 128, 0)) == _lib.PSA_ERR_UNSUPPORTED        # 10000 blocks
-    assert _attn(batch=4097) == _lib.PSA_ERR_UNSUPPORTED
+    assert _attn(batch=1025) == _lib.PSA_ERR_UNSUPPORTED
 
 
 def test_error_messages():
