@@ -7,8 +7,19 @@ tensors for the speedup.  One JSON line goes to stdout; details go to stderr.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload wan14b|wan1_3b|hunyuan|sweep]
                     [--target 0.3] [--no-dense] [--no-cpu-baseline]
+
+The roofline figure is that of the persistent sparse kernel alone (psa_attention_run over a
+planned workspace, timed with HIP events on the launch stream).  Its HBM traffic comes from two
+rocprofv3 counter runs summarised by
+
+    python bench.py --counters <FETCH_SIZE run dir> <WRITE_SIZE run dir>
+
+into profiles/; the figure is reported only while the kernel sources hash to the ones profiled.
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import math
 import os
@@ -22,6 +33,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA peak (published)
+KERNEL = "psa_sparse_kernel<128, 128>"
+COUNTERS_MD = os.path.join(ROOT, "profiles", "psa_sparse_kernel_wan14b_counters.md")
+SOURCES = ("paper_2609_37001_amd/csrc/psa_kernels.hip", "paper_2609_37001_amd/csrc/psa_launch.h",
+           "paper_2609_37001_amd/csrc/psa_api.hip", "paper_2609_37001_amd/build.py", "include/psa.h")
 WORKLOAD_TEXT = {
     "wan14b": "Wan 2.1 14B 720p attention layer: B=1, 40 heads, d=128, grid 21x45x80 (N=75600), "
               "block 128, seeded per-head stripes (kept-tile density 10-40%)",
@@ -51,21 +66,129 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--copy-mb", type=int, default=0,
                    help="run one plain device copy of this many MiB first (counter calibration)")
+    p.add_argument("--counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) and exit")
+    p.add_argument("--kernel-stats", metavar="TRACE_DIR",
+                   help="print the kernel table of a rocprofv3 --kernel-trace --stats csv run and exit")
+    p.add_argument("--copy-calibration-mb", type=int, default=1024,
+                   help="size of the --copy-mb copy in the profiled runs (for --counters)")
     return p.parse_args()
 
 
+def source_hash():
+    h = hashlib.sha256()
+    for rel in SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
 def time_calls(fn, steps, warmup, torch):
-    """Mean ms per call over `steps` calls after `warmup`, HIP events on the current stream."""
+    """Per-call ms of `steps` back-to-back calls after `warmup`: HIP events recorded on the
+    current stream (the stream every library call launches on) between consecutive calls."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
         fn()
-    end.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    return start.elapsed_time(end) / steps
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return {"mean": ev[0].elapsed_time(ev[-1]) / steps, "median": float(np.median(per)),
+            "min": float(min(per))}
+
+
+def counter_rows(run_dir, counter):
+    """{kernel name: [per-dispatch values]} of one counter in a rocprofv3 csv run directory."""
+    out = {}
+    for path in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter:
+                    out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return out
+
+
+def summarise_counters(fetch_dir, write_dir, copy_mb):
+    """Markdown summary of the two counter runs; HBM bytes of the sparse kernel per launch,
+    each counter scaled by what it reads for the plain 'copy_mb' MiB device copy."""
+    fetch, write = counter_rows(fetch_dir, "FETCH_SIZE"), counter_rows(write_dir, "WRITE_SIZE")
+
+    def pick(rows, key):
+        hits = [v for k, v in rows.items() if key in k]
+        if not hits:
+            raise SystemExit("no dispatch of %s in the counter runs" % key)
+        return hits[0]
+
+    copy_bytes = copy_mb * 1048576.0
+    f_copy, w_copy = max(pick(fetch, "copyBuffer")), max(pick(write, "copyBuffer"))
+    f_scale, w_scale = copy_bytes / (f_copy * 1024.0), copy_bytes / (w_copy * 1024.0)
+    f_k, w_k = pick(fetch, "psa_sparse_kernel"), pick(write, "psa_sparse_kernel")
+    f_mean, w_mean = sum(f_k) / len(f_k), sum(w_k) / len(w_k)
+    traffic = f_mean * 1024.0 * f_scale + w_mean * 1024.0 * w_scale
+    lines = [
+        "# HBM traffic counters: %s, Wan 2.1 14B shape" % KERNEL,
+        "",
+        "Workload: B=1, 40 heads, N=75600 (21x45x80), d=128, block 128, seeded stripes "
+        "(kept-tile density 0.238).",
+        "",
+        "Commands (repository root, MI355X; one counter pass per run):",
+        "",
+        "    cd /tmp && export TMPDIR=/tmp && cd -",
+        "    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- "
+        "python3 bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --copy-mb %d" % copy_mb,
+        "    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- "
+        "python3 bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --copy-mb %d" % copy_mb,
+        "    python3 bench.py --counters gpurun_out/pmc_fetch gpurun_out/pmc_write",
+        "",
+        "| quantity | value |",
+        "|---|---|",
+        "| copy calibration: %d MiB device copy, FETCH_SIZE | %.0f KiB (scale %.4f) |" % (copy_mb, f_copy, f_scale),
+        "| copy calibration: %d MiB device copy, WRITE_SIZE | %.0f KiB (scale %.4f) |" % (copy_mb, w_copy, w_scale),
+        "| sparse kernel dispatches | %d |" % len(f_k),
+        "| FETCH_SIZE per dispatch (raw) | %.0f KiB |" % f_mean,
+        "| WRITE_SIZE per dispatch (raw) | %.0f KiB |" % w_mean,
+        "| read bytes per launch (scaled) | %.4g |" % (f_mean * 1024.0 * f_scale),
+        "| written bytes per launch (scaled) | %.4g |" % (w_mean * 1024.0 * w_scale),
+        "",
+        "traffic_bytes_per_launch: %.6g" % traffic,
+        "source_hash: %s" % source_hash(),
+        "",
+        "Algorithmic bytes per launch: Q, K, V read once and O written once, "
+        "4 x 40 x 75600 x 128 x 2 B = 3.097e9 B.  Traffic above that is K/V tiles that missed "
+        "the L2 (each kept tile is streamed once per query block).",
+    ]
+    return "\n".join(lines) + "\n"
+
+
+def kernel_stats_table(trace_dir):
+    """Markdown table of rocprofv3's kernel_stats.csv (durations in microseconds)."""
+    paths = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not paths:
+        raise SystemExit("no kernel_stats.csv under %s" % trace_dir)
+    lines = ["| kernel | calls | total us | average us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
+    with open(paths[0]) as f:
+        for r in csv.DictReader(f):
+            name = r["Name"].split("(")[0].replace("void ", "")
+            lines.append("| %s | %s | %.1f | %.1f | %.1f | %.1f | %.2f |" % (
+                name, r["Calls"], float(r["TotalDurationNs"]) / 1e3, float(r["AverageNs"]) / 1e3,
+                float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    return "\n".join(lines) + "\n"
+
+
+def recorded_traffic():
+    """Bytes per launch of the sparse kernel from the committed counter summary, or None when
+    the summary is missing or the kernel sources changed since it was taken."""
+    try:
+        text = open(COUNTERS_MD).read()
+    except OSError:
+        return None
+    vals = dict(l.split(": ", 1) for l in text.splitlines() if l.startswith(("traffic_bytes", "source_hash")))
+    if vals.get("source_hash", "").strip() != source_hash():
+        return None
+    return float(vals["traffic_bytes_per_launch"])
 
 
 def computed_flops(psa, cfg, params, torch):
@@ -121,6 +244,12 @@ def cpu_baseline(cfg, params, seconds):
 
 def main():
     args = parse()
+    if args.kernel_stats:
+        sys.stdout.write(kernel_stats_table(args.kernel_stats))
+        return 0
+    if args.counters:
+        sys.stdout.write(summarise_counters(args.counters[0], args.counters[1], args.copy_calibration_mb))
+        return 0
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the attention "
               "kernel shards over heads; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
@@ -152,8 +281,17 @@ def main():
     def sparse():
         psa.attention_fwd(q, k, v, grid, cfg.block, params, cfg.scale, out=o, workspace=ws)
 
-    ms = time_calls(sparse, args.steps, args.warmup, torch)
+    t_step = time_calls(sparse, args.steps, args.warmup, torch)
+    ms = t_step["mean"]
     tflops = flops / (ms * 1e-3) / 1e12
+
+    # The dominant kernel alone: psa_attention_run over the plan the step above left in ws.
+    def kernel_only():
+        psa.run(q, k, v, grid, cfg.block, ws, cfg.scale, out=o)
+
+    t_kernel = time_calls(kernel_only, args.steps, 1, torch)
+    k_tflops = flops / (t_kernel["mean"] * 1e-3) / 1e12
+    props = torch.cuda.get_device_properties(0)
     dense_flops = cfg.dense_flops
     result = {
         "metric": "sparse-attn fwd computed TFLOP/s & MFU; speedup vs own dense at Wan-14B shape",
@@ -173,13 +311,22 @@ def main():
                    "dense_tflop": round(dense_flops / 1e12, 4)},
         "mfu": round(tflops / PEAK_BF16_TFLOPS, 4),
         "dense_equiv_tflops": round(dense_flops / (ms * 1e-3) / 1e12, 2),
+        "step_ms": {key: round(val, 4) for key, val in t_step.items()},
+        "kernel_ms": {key: round(val, 4) for key, val in t_kernel.items()},
+        "device": {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
+                   "compute_units": props.multi_processor_count,
+                   "hbm_gib": round(props.total_memory / 2 ** 30, 1)},
+        "seeds": {"qkv": 0, "stripes": "workloads/stripe_params.json (seeded density targeting)"},
     }
-    log("sparse: %.3f ms/step, %.1f TFLOP/s computed, MFU %.3f, density %.4f" % (ms, tflops, tflops / PEAK_BF16_TFLOPS, density))
+    log("sparse: %.3f ms/step (median %.3f, min %.3f), %.1f TFLOP/s computed, MFU %.3f, density %.4f"
+        % (ms, t_step["median"], t_step["min"], tflops, tflops / PEAK_BF16_TFLOPS, density))
+    log("sparse kernel alone: %.3f ms (median %.3f, min %.3f), %.1f TFLOP/s"
+        % (t_kernel["mean"], t_kernel["median"], t_kernel["min"], k_tflops))
     if not args.no_dense:
         def dense():
             psa.dense_fwd(q, k, v, cfg.block, cfg.scale, out=o)
         dsteps = args.dense_steps or max(3, args.steps // 2)
-        dms = time_calls(dense, dsteps, 1, torch)
+        dms = time_calls(dense, dsteps, 1, torch)["mean"]
         dtf = dense_flops / (dms * 1e-3) / 1e12
         speedup = dms / ms
         result.update({
@@ -191,13 +338,15 @@ def main():
             "speedup_over_inverse_density": round(speedup * density, 4),
         })
         log("dense: %.3f ms, %.1f TFLOP/s, speedup %.3f (x density %.3f)" % (dms, dtf, speedup, speedup * density))
+    traffic = recorded_traffic() if name == "wan14b" else None
     result["roofline"] = {
+        "kernel": KERNEL,
         "bound": "mfma",
-        "achieved": round(tflops, 2),
+        "achieved": round(k_tflops, 2),
         "peak": PEAK_BF16_TFLOPS,
         "unit": "TFLOP/s",
-        "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-        "traffic": None,
+        "frac": round(k_tflops / PEAK_BF16_TFLOPS, 4),
+        "traffic": traffic,
     }
     if not args.no_cpu_baseline:
         log("cpu baseline: timing the oracle for about %.0f s" % args.cpu_seconds)

@@ -85,9 +85,10 @@ typedef enum {
 /* Number of blocks ceil(N / block) of the grid, or -1 if grid or block is invalid. */
 int32_t psa_num_blocks(psa_grid_t grid, int32_t block);
 
-/* Bytes of device workspace psa_attention_fwd needs for these sizes (0 if invalid).
- * The workspace holds the decoded per-head parameters, the kept-block count of every
- * (batch, head, query block) work item, the load-balanced work order and queue counters. */
+/* Bytes of device workspace psa_attention_plan / psa_attention_fwd need for these sizes
+ * (0 if invalid).  The workspace holds a plan: the per-head parameters, the block coordinates,
+ * the kept-block count of every (batch, head, query block) work item, the load-balanced work
+ * order, the queue counters and a header naming the sizes the plan was made for. */
 size_t psa_workspace_size(int32_t batch, int32_t n_heads, psa_grid_t grid, int32_t block);
 
 /* Block map of Algorithm 1 at block granularity (Sec. 3.2), computed on the device by the same
@@ -101,8 +102,36 @@ psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa
                                 int32_t block, uint8_t* blockmap, int32_t* kept_per_row,
                                 int64_t* kept_per_head, hipStream_t stream);
 
+/* Plan of psa_attention_run (the work list of Algorithm 2 without the attention itself): copies
+ * the stripe parameters of each head to the workspace, counts the kept key blocks of every
+ * (batch, head, query block) work item with the Algorithm 1 decoder, orders the items longest
+ * head first and splits each head into equal-work ranges, one work queue per XCD.  The plan
+ * depends only on the sizes and on params, so one plan serves any number of runs (a layer's
+ * stripes stay fixed over the denoising steps).
+ *   workspace     device, psa_workspace_size(batch, n_heads, grid, block) bytes or more,
+ *                 256-byte aligned; owned by the caller, overwritten
+ *   kept_per_row  device int32 [n_heads][nb]: kept key blocks of each query block, or NULL
+ * Limits: nb <= PSA_MAX_BLOCKS, batch * n_heads <= PSA_MAX_BATCH_HEADS, block 64 or 128. */
+psa_status_t psa_attention_plan(int32_t batch, int32_t n_heads, psa_grid_t grid, int32_t block,
+                                const psa_stripe_t* params, void* workspace,
+                                size_t workspace_bytes, int32_t* kept_per_row,
+                                hipStream_t stream);
+
+/* Sparse attention over a planned workspace (Algorithm 2): one persistent kernel whose
+ * workgroups pop query blocks from the plan's queues, decode each one's kept key blocks
+ * (Algorithm 1) and run the tile engine over them.  Arguments as in psa_attention_fwd.  The
+ * workspace must hold a plan made for the same batch, n_heads, grid and block; the kernel checks
+ * the plan's header first and, on a mismatch or an unfinished plan, writes nothing (o and lse keep
+ * their contents; no error can be returned for a condition found on the device).  The run uses
+ * the plan's queue counters and re-arms them before it ends, so runs over one workspace must not
+ * overlap in time (use one workspace per stream). */
+psa_status_t psa_attention_run(const void* q, const void* k, const void* v, void* o,
+                               int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
+                               int32_t block, float softmax_scale, void* workspace,
+                               size_t workspace_bytes, float* lse, hipStream_t stream);
+
 /* PSA block-sparse attention forward (Algorithm 2): o = softmax(scale * q k^T restricted to the
- * kept blocks of each head) v.
+ * kept blocks of each head) v.  Equivalent to psa_attention_plan followed by psa_attention_run.
  *   q, k, v, o     device bf16 [batch][n_heads][N][head_dim]; N = frames*height*width + n_text
  *   head_dim       64 or 128;  block: 64 or 128 (query and key block size, the tile size)
  *   params         host [n_heads]; the same M for every batch element

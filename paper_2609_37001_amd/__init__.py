@@ -8,6 +8,8 @@ is no CPU or PyTorch fallback.
     params = [(T_w, T_o, T_s, S_w, S_o, S_s), ...]          # one 6-tuple per head
     o = attention_fwd(q, k, v, grid=(F, H, W, n_text), block=128, params=params)
     o_dense = dense_fwd(q, k, v, block=128)
+    ws = plan(params, grid, block, batch=1)                   # plan once ...
+    o = run(q, k, v, grid, block, ws)                         # ... run many times
     bmap, per_row, per_head = build_blockmap(params, (F, H, W, n_text), block=128)
 """
 import math
@@ -16,7 +18,7 @@ from . import _lib
 from ._lib import STRIDE_INF, PsaError  # noqa: F401
 
 __all__ = ["STRIDE_INF", "PsaError", "num_blocks", "workspace_size", "build_blockmap",
-           "attention_fwd", "dense_fwd", "Workspace", "library_path"]
+           "attention_fwd", "plan", "run", "dense_fwd", "Workspace", "library_path"]
 
 
 def library_path():
@@ -78,7 +80,9 @@ def _check_qkv(*ts):
 
 
 class Workspace:
-    """Device workspace for attention_fwd (a byte tensor on the given device)."""
+    """Device workspace for attention_fwd / plan / run (a byte tensor on the given device).
+
+    After plan() it also records the sizes and parameters of the plan it holds."""
 
     def __init__(self, batch, n_heads, grid, block, device):
         torch = _torch()
@@ -86,6 +90,13 @@ class Workspace:
         if self.nbytes == 0:
             raise ValueError("invalid sizes for a workspace")
         self.tensor = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+        self.sizes = (int(batch), int(n_heads), tuple(int(x) for x in _grid_tuple(grid)), int(block))
+        self.params = None
+
+
+def _grid_tuple(grid):
+    g = tuple(int(x) for x in grid)
+    return g + (0,) if len(g) == 3 else g
 
 
 def build_blockmap(params, grid, block, device=None, blockmap=True, per_row=True, per_head=True,
@@ -131,12 +142,56 @@ def attention_fwd(q, k, v, grid, block, params, scale=None, out=None, return_lse
             _ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, _grid(grid), int(block),
             _lib.stripes(params), scale, _ptr(ws.tensor), ws.nbytes, _ptr(lse), _ptr(kept),
             _stream(stream, q.device)))
+    ws.sizes = (b, h, _grid_tuple(grid), int(block))
+    ws.params = [tuple(int(x) for x in m) for m in params]
     res = (o,)
     if return_lse:
         res += (lse,)
     if return_kept_per_row:
         res += (kept,)
     return res[0] if len(res) == 1 else res
+
+
+def plan(params, grid, block, batch=1, device=None, workspace=None, return_kept_per_row=False,
+         stream=None):
+    """Plan of the sparse attention for these stripes and sizes (psa_attention_plan).
+
+    Returns the Workspace holding it (and kept_per_row int32 [heads, nb] if asked)."""
+    torch = _torch()
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    h = len(params)
+    ws = workspace if workspace is not None else Workspace(batch, h, grid, block, device)
+    nb = num_blocks(grid, block)
+    kept = torch.empty((h, max(nb, 1)), dtype=torch.int32, device=device) if return_kept_per_row else None
+    with torch.cuda.device(device):
+        _lib.check(_lib.lib().psa_attention_plan(int(batch), h, _grid(grid), int(block),
+                                                 _lib.stripes(params), _ptr(ws.tensor), ws.nbytes,
+                                                 _ptr(kept), _stream(stream, device)))
+    ws.sizes = (int(batch), h, _grid_tuple(grid), int(block))
+    ws.params = [tuple(int(x) for x in m) for m in params]
+    return (ws, kept) if return_kept_per_row else ws
+
+
+def run(q, k, v, grid, block, workspace, scale=None, out=None, return_lse=False, stream=None):
+    """Sparse attention over a planned workspace (psa_attention_run)."""
+    torch = _torch()
+    _check_qkv(q, k, v)
+    b, h, n, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q) if out is None else out
+    _check_qkv(q, o)
+    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+    ws = workspace
+    if ws.params is None:
+        raise ValueError("the workspace holds no plan: call plan() or attention_fwd() first")
+    if ws.sizes != (b, h, _grid_tuple(grid), int(block)):
+        raise ValueError("the workspace was planned for (batch, heads, grid, block) = %s, not %s"
+                         % (ws.sizes, (b, h, _grid_tuple(grid), int(block))))
+    with torch.cuda.device(q.device):
+        _lib.check(_lib.lib().psa_attention_run(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, _grid(grid), int(block), scale,
+            _ptr(ws.tensor), ws.nbytes, _ptr(lse), _stream(stream, q.device)))
+    return (o, lse) if return_lse else o
 
 
 def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=None):

@@ -21,8 +21,9 @@ PSA_ERR_UNSUPPORTED = 2
 PSA_ERR_WORKSPACE = 3
 PSA_ERR_HIP = 4
 
-EXPORTS = ("psa_num_blocks", "psa_workspace_size", "psa_build_blockmap", "psa_attention_fwd",
-           "psa_dense_fwd", "psa_status_string", "psa_last_error")
+EXPORTS = ("psa_num_blocks", "psa_workspace_size", "psa_build_blockmap", "psa_attention_plan",
+           "psa_attention_run", "psa_attention_fwd", "psa_dense_fwd", "psa_status_string",
+           "psa_last_error")
 
 
 class Stripe(ctypes.Structure):
@@ -58,6 +59,10 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError("libpsa.so is not built: run `python -m paper_2609_37001_amd.build`")
+        # torch ships its own HIP runtime under the soname libamdhip64.so.7; whichever copy is
+        # loaded first serves the whole process.  Loading torch first makes the library bind to
+        # the runtime that owns the tensors and streams it is handed.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         L.psa_num_blocks.argtypes = [Grid, i32]
@@ -66,6 +71,11 @@ def lib():
         L.psa_workspace_size.restype = sz
         L.psa_build_blockmap.argtypes = [ctypes.POINTER(Stripe), i32, Grid, i32, vp, vp, vp, vp]
         L.psa_build_blockmap.restype = ctypes.c_int
+        L.psa_attention_plan.argtypes = [i32, i32, Grid, i32, ctypes.POINTER(Stripe), vp, sz, vp, vp]
+        L.psa_attention_plan.restype = ctypes.c_int
+        L.psa_attention_run.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, i32, ctypes.c_float, vp,
+                                        sz, vp, vp]
+        L.psa_attention_run.restype = ctypes.c_int
         L.psa_attention_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, i32,
                                         ctypes.POINTER(Stripe), ctypes.c_float, vp, sz, vp, vp, vp]
         L.psa_attention_fwd.restype = ctypes.c_int

@@ -74,6 +74,33 @@ psa_status_t check_attention_shape(int32_t batch, int32_t n_heads, int32_t head_
   return PSA_OK;
 }
 
+// Sizes shared by the plan and the run: grid, limits of the scheduler and the workspace.
+psa_status_t check_plan(int32_t batch, int32_t n_heads, psa_grid_t grid, int32_t block,
+                        const void* workspace, size_t workspace_bytes, psa::Geometry* g,
+                        psa::WorkspaceLayout* wl) {
+  if (batch < 1) return fail(PSA_ERR_INVALID, "batch must be >= 1 (got %d)", batch);
+  if (n_heads < 1) return fail(PSA_ERR_INVALID, "n_heads must be >= 1 (got %d)", n_heads);
+  if (block != 64 && block != 128)
+    return fail(PSA_ERR_UNSUPPORTED, "block must be 64 or 128 (got %d)", block);
+  if (!grid_geometry(grid, block, g))
+    return fail(PSA_ERR_INVALID, "invalid grid (%d x %d x %d + %d text)", grid.frames, grid.height,
+                grid.width, grid.n_text);
+  if (g->nb > PSA_MAX_BLOCKS)
+    return fail(PSA_ERR_UNSUPPORTED, "%d blocks per sequence exceed %d", g->nb, PSA_MAX_BLOCKS);
+  if ((int64_t)batch * n_heads > PSA_MAX_BATCH_HEADS)
+    return fail(PSA_ERR_UNSUPPORTED, "batch*n_heads = %lld exceeds %d", (long long)batch * n_heads,
+                PSA_MAX_BATCH_HEADS);
+  if ((int64_t)batch * n_heads * g->nb >= ((int64_t)1 << 31))
+    return fail(PSA_ERR_UNSUPPORTED, "too many work items");
+  *wl = psa::workspace_layout(batch, n_heads, g->nb);
+  if (!workspace || workspace_bytes < wl->total)
+    return fail(PSA_ERR_WORKSPACE, "workspace of %zu bytes at %p; %zu bytes required", workspace_bytes,
+                workspace, wl->total);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(PSA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return PSA_OK;
+}
+
 int32_t persistent_workgroups() {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
@@ -116,6 +143,44 @@ psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa
   return PSA_OK;
 }
 
+psa_status_t psa_attention_plan(int32_t batch, int32_t n_heads, psa_grid_t grid, int32_t block,
+                                const psa_stripe_t* params, void* workspace,
+                                size_t workspace_bytes, int32_t* kept_per_row,
+                                hipStream_t stream) {
+  psa::Geometry g;
+  psa::WorkspaceLayout wl;
+  psa_status_t s = check_plan(batch, n_heads, grid, block, workspace, workspace_bytes, &g, &wl);
+  if (s != PSA_OK) return s;
+  s = check_params(params, n_heads);
+  if (s != PSA_OK) return s;
+  for (int32_t h0 = 0; h0 < n_heads; h0 += psa::kHeadsPerChunk) {
+    const psa::ParamChunk pc = chunk_of(params, h0, n_heads);
+    hipError_t e = psa::launch_setup(pc, h0, g, workspace, wl, h0 == 0, stream);
+    if (e != hipSuccess) return hip_fail(e, "psa_attention_plan setup launch");
+  }
+  hipError_t e = psa::launch_schedule(g, batch, n_heads, workspace, wl, kept_per_row, stream);
+  if (e != hipSuccess) return hip_fail(e, "psa_attention_plan schedule launch");
+  return PSA_OK;
+}
+
+psa_status_t psa_attention_run(const void* q, const void* k, const void* v, void* o,
+                               int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
+                               int32_t block, float softmax_scale, void* workspace,
+                               size_t workspace_bytes, float* lse, hipStream_t stream) {
+  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
+  psa_status_t s = check_attention_shape(batch, n_heads, head_dim, block);
+  if (s != PSA_OK) return s;
+  psa::Geometry g;
+  psa::WorkspaceLayout wl;
+  s = check_plan(batch, n_heads, grid, block, workspace, workspace_bytes, &g, &wl);
+  if (s != PSA_OK) return s;
+  const float c = softmax_scale * 1.4426950408889634f;
+  hipError_t e = psa::launch_sparse(q, k, v, o, lse, batch, n_heads, head_dim, g, c, workspace, wl,
+                                    persistent_workgroups(), stream);
+  if (e != hipSuccess) return hip_fail(e, "psa_attention_run kernel launch");
+  return PSA_OK;
+}
+
 psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void* o,
                                int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
                                int32_t block, const psa_stripe_t* params, float softmax_scale,
@@ -124,38 +189,11 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
   if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
   psa_status_t s = check_attention_shape(batch, n_heads, head_dim, block);
   if (s != PSA_OK) return s;
-  psa::Geometry g;
-  if (!grid_geometry(grid, block, &g))
-    return fail(PSA_ERR_INVALID, "invalid grid (%d x %d x %d + %d text)", grid.frames, grid.height,
-                grid.width, grid.n_text);
-  s = check_params(params, n_heads);
+  s = psa_attention_plan(batch, n_heads, grid, block, params, workspace, workspace_bytes,
+                         kept_per_row, stream);
   if (s != PSA_OK) return s;
-  if (g.nb > PSA_MAX_BLOCKS)
-    return fail(PSA_ERR_UNSUPPORTED, "%d blocks per sequence exceed %d", g.nb, PSA_MAX_BLOCKS);
-  if ((int64_t)batch * n_heads > PSA_MAX_BATCH_HEADS)
-    return fail(PSA_ERR_UNSUPPORTED, "batch*n_heads = %lld exceeds %d", (long long)batch * n_heads,
-                PSA_MAX_BATCH_HEADS);
-  if ((int64_t)batch * n_heads * g.nb >= ((int64_t)1 << 31))
-    return fail(PSA_ERR_UNSUPPORTED, "too many work items");
-  const psa::WorkspaceLayout wl = psa::workspace_layout(batch, n_heads, g.nb);
-  if (!workspace || workspace_bytes < wl.total)
-    return fail(PSA_ERR_WORKSPACE, "workspace of %zu bytes at %p; %zu bytes required", workspace_bytes,
-                workspace, wl.total);
-  if (((uintptr_t)workspace & 255) != 0)
-    return fail(PSA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-
-  for (int32_t h0 = 0; h0 < n_heads; h0 += psa::kHeadsPerChunk) {
-    const psa::ParamChunk pc = chunk_of(params, h0, n_heads);
-    hipError_t e = psa::launch_setup(pc, h0, g, workspace, wl, h0 == 0, stream);
-    if (e != hipSuccess) return hip_fail(e, "psa_attention_fwd setup launch");
-  }
-  hipError_t e = psa::launch_schedule(g, batch, n_heads, workspace, wl, kept_per_row, stream);
-  if (e != hipSuccess) return hip_fail(e, "psa_attention_fwd schedule launch");
-  const float c = softmax_scale * 1.4426950408889634f;
-  e = psa::launch_sparse(q, k, v, o, lse, batch, n_heads, head_dim, g, c, workspace, wl,
-                         persistent_workgroups(), stream);
-  if (e != hipSuccess) return hip_fail(e, "psa_attention_fwd kernel launch");
-  return PSA_OK;
+  return psa_attention_run(q, k, v, o, batch, n_heads, head_dim, grid, block, softmax_scale,
+                           workspace, workspace_bytes, lse, stream);
 }
 
 psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o, int32_t batch,

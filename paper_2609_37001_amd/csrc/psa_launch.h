@@ -31,13 +31,34 @@ struct Geometry {
   int32_t nb;       // ceil(n / block)
 };
 
-// Workspace of psa_attention_fwd (byte offsets, each 256-aligned).
+// Identifies a finished plan in the workspace header; the sizes it was made for follow it.
+constexpr uint32_t kPlanMagic = 0x50534131u;  // "PSA1"
+
+struct PlanHeader {
+  uint32_t magic;   // kPlanMagic once psa_attention_plan's kernels have run, 0 while they run
+  int32_t n_bh;     // batch * n_heads
+  int32_t n_heads;
+  int32_t nb;
+  int32_t block;
+  int32_t n;
+  int32_t hw;
+  int32_t n_text;
+};
+
+// Layout of the queue area: kNumQueues + 1 boundaries, kNumQueues pop counters, one exit
+// counter.
+constexpr int kQueueCounters = kNumQueues + 1;
+constexpr int kQueueDone = 2 * kNumQueues + 1;
+constexpr int kQueueWords = 2 * kNumQueues + 2;
+
+// Workspace of psa_attention_plan / psa_attention_run (byte offsets, each 256-aligned).
 struct WorkspaceLayout {
+  size_t header;    // PlanHeader
   size_t params;    // psa_stripe_t [n_heads]
   size_t coords;    // int2 [nb]: (frame, slot) of each block, frame = -1 for a global block
   size_t counts;    // int32 [batch*n_heads*nb]: kept key blocks per work item
   size_t order;     // int32 [batch*n_heads*nb]: work items in schedule order
-  size_t queues;    // int32 [2*kNumQueues+1]: queue boundaries then queue counters
+  size_t queues;    // int32 [kQueueWords]: queue boundaries, pop counters, exit counter
   size_t total;
 };
 
@@ -51,6 +72,7 @@ hipError_t launch_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& 
 hipError_t launch_setup(const ParamChunk& pc, int32_t head0, const Geometry& g, void* workspace,
                         const WorkspaceLayout& wl, bool write_coords, hipStream_t stream);
 
+// Counts the kept blocks of every work item, orders them, and writes the header last.
 hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, void* workspace,
                            const WorkspaceLayout& wl, int32_t* kept_per_row, hipStream_t stream);
 

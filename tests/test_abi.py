@@ -98,3 +98,41 @@ def test_blockmap_validation_codes():
     assert L.psa_build_blockmap(_lib.stripes([(1, 0, 1, 1, 0, 1)]), 1, _lib.grid_of(2, 2, 0), 1,
                                 None, None, None, None) == _lib.PSA_ERR_INVALID
     assert L.psa_build_blockmap(None, 1, _lib.grid_of(2, 2, 2), 1, None, None, None, None) == _lib.PSA_ERR_INVALID
+
+
+def _plan(batch=1, heads=1, grid=(2, 8, 8, 0), block=128, params=None, ws=1, wsb=1 << 20):
+    L = _lib.lib()
+    params = [(1, 0, INF, 1, 0, INF)] * heads if params is None else params
+    vp = lambda x: ctypes.c_void_p(x) if x else None
+    return L.psa_attention_plan(batch, heads, _lib.grid_of(*grid), block, _lib.stripes(params),
+                                vp(ws * 256), wsb, None, None)
+
+
+def _run(q=1, o=1, batch=1, heads=1, d=128, grid=(2, 8, 8, 0), block=128, ws=1, wsb=1 << 20):
+    L = _lib.lib()
+    vp = lambda x: ctypes.c_void_p(x) if x else None
+    return L.psa_attention_run(vp(q), vp(256), vp(256), vp(o), batch, heads, d, _lib.grid_of(*grid),
+                               block, 0.1, vp(ws * 256), wsb, None, None)
+
+
+def test_plan_validation_codes():
+    assert _plan(batch=0) == _lib.PSA_ERR_INVALID
+    assert _plan(heads=0, params=[(1, 0, 1, 1, 0, 1)]) == _lib.PSA_ERR_INVALID
+    assert _plan(block=32) == _lib.PSA_ERR_UNSUPPORTED
+    assert _plan(grid=(2, 8, 0, 0)) == _lib.PSA_ERR_INVALID
+    assert _plan(params=[(1, 0, 1, 1, 0, 0)]) == _lib.PSA_ERR_INVALID
+    assert _plan(ws=0) == _lib.PSA_ERR_WORKSPACE
+    assert _plan(wsb=8) == _lib.PSA_ERR_WORKSPACE
+    assert _plan(ws=1, wsb=1 << 20, grid=(100, 100, 128, 0)) == _lib.PSA_ERR_UNSUPPORTED
+    assert _plan(batch=33, heads=32, params=[(1, 0, 1, 1, 0, 1)] * 32) == _lib.PSA_ERR_UNSUPPORTED
+
+
+def test_run_validation_codes():
+    assert _run(q=0) == _lib.PSA_ERR_INVALID
+    assert _run(o=0) == _lib.PSA_ERR_INVALID
+    assert _run(d=96) == _lib.PSA_ERR_UNSUPPORTED
+    assert _run(block=16) == _lib.PSA_ERR_UNSUPPORTED
+    assert _run(heads=0) == _lib.PSA_ERR_INVALID
+    assert _run(ws=0) == _lib.PSA_ERR_WORKSPACE
+    assert _run(wsb=100) == _lib.PSA_ERR_WORKSPACE
+

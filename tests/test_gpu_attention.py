@@ -125,3 +125,56 @@ def test_constant_values_and_empty_rows():
     lse = lse.cpu().numpy()[0, 0]
     assert (o[: 3 * 128] == 1.0).all()
     assert (o[3 * 128:] == 0).all() and np.isneginf(lse[3 * 128:]).all()
+
+
+def test_plan_once_run_many_equals_fwd():
+    """One plan serves repeated runs (the queue counters re-arm): every run returns the bits of
+    attention_fwd, for two different inputs over the same plan."""
+    torch = gu.torch()
+    f, hh, ww, nt = 3, 10, 13, 37
+    params = [(2, 0, INF, 3, 1, 5), (1, 0, 2, 2, -1, 3), (1, 1, INF, 1, 0, INF)]
+    grid = (f, hh, ww, nt)
+    ws, kept = psa.plan(params, grid, 64, batch=2, return_kept_per_row=True)
+    keep = oracle.blockmap(params, f, hh, ww, nt, 64)
+    assert (kept.cpu().numpy() == oracle.kept_per_row(keep)).all()
+    for seed in (3, 4):
+        q, k, v = (dev(x) for x in random_problem(2, 3, f * hh * ww + nt, 128, seed=seed))
+        ref, lref = psa.attention_fwd(q, k, v, grid, 64, params, 0.1, return_lse=True)
+        for _ in range(3):
+            o, l = psa.run(q, k, v, grid, 64, ws, 0.1, return_lse=True)
+            torch.cuda.synchronize()
+            assert torch.equal(o, ref) and torch.equal(l, lref)
+
+
+def test_run_without_matching_plan_writes_nothing():
+    """The kernel checks the plan header: an unplanned workspace, or one planned for another
+    grid, leaves o and lse untouched (checked through the C ABI, past the binding's own check)."""
+    import ctypes
+    from paper_2609_37001_amd import _lib
+    torch = gu.torch()
+    grid, other = (2, 8, 16, 0), (2, 8, 16, 5)
+    n = 2 * 8 * 16
+    q, k, v = (dev(x) for x in random_problem(1, 1, n, 128, seed=9))
+    size = max(psa.workspace_size(1, 1, grid, 128), psa.workspace_size(1, 1, other, 128))
+    vp = lambda t: ctypes.c_void_p(t.data_ptr())
+
+    def raw_run(ws, o, lse):
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        return _lib.lib().psa_attention_run(vp(q), vp(k), vp(v), vp(o), 1, 1, 128,
+                                            _lib.grid_of(*grid), 128, 0.1, vp(ws), size, vp(lse), stream)
+
+    ws = torch.zeros(size, dtype=torch.uint8, device="cuda:0")          # no plan at all
+    o = torch.full_like(q, 7.0)
+    lse = torch.full((1, 1, n), 3.0, device="cuda:0")
+    assert raw_run(ws, o, lse) == _lib.PSA_OK
+    torch.cuda.synchronize()
+    assert (o == 7.0).all() and (lse == 3.0).all()
+    params = [(1, 0, INF, 1, 0, INF)]
+    assert _lib.lib().psa_attention_plan(1, 1, _lib.grid_of(*other), 128, _lib.stripes(params),
+                                         vp(ws), size, None,
+                                         ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)) == 0
+    assert raw_run(ws, o, lse) == _lib.PSA_OK                           # planned for 5 text tokens
+    torch.cuda.synchronize()
+    assert (o == 7.0).all() and (lse == 3.0).all()
+    with pytest.raises(ValueError):
+        psa.run(q, k, v, grid, 128, psa.Workspace(1, 1, grid, 128, "cuda:0"))
