@@ -33,9 +33,10 @@
  *  - The library holds no allocation and no mutable global state apart from the thread-local
  *    error message; calls are re-entrant.  Two calls that share an output or a workspace must
  *    not overlap in time.
- *  - Numerics: bf16 x bf16 products accumulated in fp32 (MFMA); softmax statistics in fp32;
- *    P rounded to bf16 before P V; O rounded to bf16 (round to nearest even).  A query row with
- *    no kept key gets O = 0 and LSE = -inf.
+ *  - Numerics: q is multiplied by softmax_scale * log2(e) and rounded to bf16 once; bf16 x bf16
+ *    products accumulated in fp32 (MFMA); softmax statistics in fp32 in the exp2 domain; P
+ *    rounded to bf16 before P V, and the normaliser sums the rounded P; O rounded to bf16 (round
+ *    to nearest even).  A query row with no kept key gets O = 0 and LSE = -inf.
  */
 #ifndef PSA_H
 #define PSA_H

@@ -33,6 +33,7 @@
 namespace psa {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
@@ -445,13 +446,17 @@ __device__ __forceinline__ void issue_block(const DmaPlan<D, BLK>& plan, const _
 }
 
 // Per-wave state: 32 query rows (lane l owns row l & 31; lanes l and l^32 split its keys).
+// Scores live in the exp2 domain: Q is multiplied by scale*log2(e) once, when it is loaded, and
+// the S^T accumulators start at -m instead of 0, so the MFMAs deliver S - m and the softmax needs
+// no per-score multiply or subtract.
 template <int D, int BLK>
 struct WaveState {
   using T = Tile<D, BLK>;
-  bf16x8 q[T::DC];     // Q^T B operands
+  bf16x8 q[T::DC];     // (scale*log2(e) Q)^T B operands
   f32x16 o[T::DT];     // O^T accumulators
-  float m;             // running max, scaled by scale*log2(e)
-  float l;             // running sum over this lane's keys
+  f32x16 negm;         // -m in all 16 elements (0 while m = -inf): initial S^T accumulator
+  float m;             // running max of the scaled scores
+  float l;             // running sum of the bf16-rounded P over this lane's keys
 };
 
 // Each key/value block is processed in two halves of HK = BLK/2 keys (S^T: HK/32 groups of 32 keys
@@ -474,14 +479,12 @@ __device__ __forceinline__ void qk_half(const WaveState<D, BLK>& st,
   const int krow0 = k0 + key_perm(lane & 31);
   const int ksw = swz<T::CPR>(krow0);   // identical for krow0 + 32 kt
 #pragma unroll
-  for (int kt = 0; kt < H::KT; kt++) s[kt] = (f32x16){};
-#pragma unroll
   for (int cc = 0; cc < T::DC; cc++) {
 #pragma unroll
     for (int kt = 0; kt < H::KT; kt++) {
       const bf16x8 a =
           *(const bf16x8*)(sk + (krow0 + 32 * kt) * T::RB + (((2 * cc + h) ^ ksw) << 4));
-      s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, st.q[cc], s[kt], 0, 0, 0);
+      s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, st.q[cc], cc == 0 ? st.negm : s[kt], 0, 0, 0);
     }
   }
 }
@@ -496,7 +499,7 @@ __device__ __forceinline__ void qk_half(const WaveState<D, BLK>& st,
 template <int D, int BLK>
 __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
                                                 f32x16 (&s)[Half<D, BLK>::KT], const uint8_t* sv,
-                                                int kb, int k0, int n, float c, bool tail,
+                                                int kb, int k0, int n, bool tail,
                                                 int lane) {
   using T = Tile<D, BLK>;
   using H = Half<D, BLK>;
@@ -511,35 +514,45 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
         if (kbase + kt * 32 + 16 * (i >> 3) + (i & 7) >= n) s[kt][i] = -__builtin_inff();
   }
 
+  // s holds S - base with base = -negm (the running max, or 0 before the first kept key).
   float mx = -__builtin_inff();
 #pragma unroll
   for (int kt = 0; kt < H::KT; kt++)
 #pragma unroll
     for (int i = 0; i < 16; i++) mx = fmaxf(mx, s[kt][i]);
-  const float ms = pair_max(mx) * c;
+  const float base = -st.negm[0];
+  const float ms = pair_max(mx) + base;
   const bool need = ms - st.m > 8.0f;     // false for -inf - -inf (NaN)
   if (__builtin_amdgcn_ballot_w64(need)) {
     asm volatile("" ::: "memory");        // keep this rare path a branch
     const float alpha = need ? __builtin_amdgcn_exp2f(st.m - ms) : 1.0f;
+    const float shift = need ? ms - base : 0.0f;
     st.m = need ? ms : st.m;
     st.l *= alpha;
 #pragma unroll
     for (int dt = 0; dt < T::DT; dt++) st.o[dt] *= alpha;
+#pragma unroll
+    for (int kt = 0; kt < H::KT; kt++) s[kt] -= shift;
+    const float nb = st.m == -__builtin_inff() ? 0.0f : -st.m;
+#pragma unroll
+    for (int i = 0; i < 16; i++) st.negm[i] = nb;
   }
-  const float base = st.m == -__builtin_inff() ? 0.0f : st.m;
 
   const int vkey = k0 + 8 * h + (j16 >> 2);
   const int vsw0 = swz<T::CPR>(vkey), vsw1 = swz<T::CPR>(vkey + 4);   // identical for vkey + 16 j
-  float sum[2] = {0.0f, 0.0f};
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
   for (int j = 0; j < H::KC; j++) {
     f32x8 e;
 #pragma unroll
-    for (int x = 0; x < 8; x++) {
-      e[x] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j >> 1][8 * (j & 1) + x], c, -base));
-      sum[x & 1] += e[x];
-    }
+    for (int x = 0; x < 8; x++) e[x] = __builtin_amdgcn_exp2f(s[j >> 1][8 * (j & 1) + x]);
     const bf16x8 p = __builtin_convertvector(e, bf16x8);
+    // Row sum of the rounded weights, two per instruction: the normaliser matches the P that
+    // multiplies V.
+    st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 0, 1), ones, st.l, false);
+    st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 2, 3), ones, st.l, false);
+    st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 4, 5), ones, st.l, false);
+    st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 6, 7), ones, st.l, false);
 #pragma unroll
     for (int dt = 0; dt < T::DT; dt++) {
       const int dd = dt * 32 + 16 * (g & 1) + 4 * (j16 & 3);
@@ -552,7 +565,6 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
       st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p, st.o[dt], 0, 0, 0);
     }
   }
-  st.l += sum[0] + sum[1];
 }
 
 // One key/value block with a single K and a single V buffer per workgroup:
@@ -563,7 +575,7 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
 template <int D, int BLK>
 __device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<D, BLK>& plan,
                                            const __bf16* kh, const __bf16* vh, int kb, int kb_next,
-                                           int n, float c, const uint8_t* sk, const uint8_t* sv,
+                                           int n, const uint8_t* sk, const uint8_t* sv,
                                            int lane) {
   const bool tail = (kb + 1) * BLK > n;
   using H = Half<D, BLK>;
@@ -571,11 +583,11 @@ __device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<
   qk_half<D, BLK>(st, s, sk, 0, lane);
   wait_dma<0>();
   __syncthreads();
-  softmax_pv_half<D, BLK>(st, s, sv, kb, 0, n, c, tail, lane);
+  softmax_pv_half<D, BLK>(st, s, sv, kb, 0, n, tail, lane);
   qk_half<D, BLK>(st, s, sk, H::HK, lane);
   __syncthreads();
   if (kb_next >= 0) issue_block<D, BLK>(plan, kh, plan.lds_k, kb_next, n);
-  softmax_pv_half<D, BLK>(st, s, sv, kb, H::HK, n, c, tail, lane);
+  softmax_pv_half<D, BLK>(st, s, sv, kb, H::HK, n, tail, lane);
   wait_dma<0>();
   __syncthreads();
   if (kb_next >= 0) issue_block<D, BLK>(plan, vh, plan.lds_v, kb_next, n);
@@ -601,14 +613,18 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
     const bf16x8* src = (const bf16x8*)(qh + (size_t)min(row, n - 1) * D) + h;
 #pragma unroll
     for (int cc = 0; cc < T::DC; cc++) st.q[cc] = src[2 * cc];
-    // Consume the Q registers here: the compiler then waits for these loads once, before any
-    // K/V DMA is issued, instead of inside the block loop where the hardware counter also
-    // counts the in-flight DMA.
+    // Scaling consumes the Q registers here: the compiler then waits for these loads once,
+    // before any K/V DMA is issued, instead of inside the block loop where the hardware counter
+    // also counts the in-flight DMA.
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++)
+      st.q[cc] = __builtin_convertvector(__builtin_convertvector(st.q[cc], f32x8) * c, bf16x8);
 #pragma unroll
     for (int cc = 0; cc < T::DC; cc++) asm volatile("" ::"v"(st.q[cc]));
   }
   st.m = -__builtin_inff();
   st.l = 0.0f;
+  st.negm = (f32x16){};
 #pragma unroll
   for (int dt = 0; dt < T::DT; dt++) st.o[dt] = (f32x16){};
 
@@ -624,7 +640,7 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
   for (int it = 0; it < nkv; it++) {
     const int kb = kv(it);
     const int kb_next = it + 1 < nkv ? kv(it + 1) : -1;
-    block_step<D, BLK>(st, plan, kh, vh, kb, kb_next, n, c, sk, sv, lane);
+    block_step<D, BLK>(st, plan, kh, vh, kb, kb_next, n, sk, sv, lane);
   }
 
   // Epilogue: O = O^T / l, rows past the end are not stored.

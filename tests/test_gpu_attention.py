@@ -21,12 +21,15 @@ def dev(x):
 
 
 def full_compare(q, k, v, keep, block, scale, o, lse):
-    """Every row of a [B, H, N, d] problem against the oracle."""
+    """Every row of a [B, H, N, d] problem against the oracle (O on the inputs as given, LSE on
+    the kernel's rounded operand, see gpu_util.kernel_q)."""
     b, h, n, d = q.shape
     num = den = mx = mlse = 0.0
     for bi in range(b):
         for hi in range(h):
-            o_ref, l_ref = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale)
+            o_ref, _ = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale)
+            _, l_ref = oracle.masked_attention(gu.kernel_q(q[bi, hi], scale), k[bi, hi], v[bi, hi],
+                                               keep[hi], block, gu.LN2)
             og = o[bi, hi].float().cpu().numpy().astype(np.float64)
             num += ((og - o_ref) ** 2).sum()
             den += (o_ref ** 2).sum()
