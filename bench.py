@@ -70,6 +70,9 @@ def parse():
                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) and exit")
     p.add_argument("--kernel-stats", metavar="TRACE_DIR",
                    help="print the kernel table of a rocprofv3 --kernel-trace --stats csv run and exit")
+    p.add_argument("--utilisation", nargs=3, metavar=("SQ_DIR", "TCC_DIR", "TRACE_DIR"),
+                   help="print utilisation figures of the attention kernels from two rocprofv3 "
+                        "--pmc runs and a kernel trace, and exit")
     p.add_argument("--copy-calibration-mb", type=int, default=1024,
                    help="size of the --copy-mb copy in the profiled runs (for --counters)")
     return p.parse_args()
@@ -178,6 +181,41 @@ def kernel_stats_table(trace_dir):
     return "\n".join(lines) + "\n"
 
 
+def utilisation_rows(sq_dir, tcc_dir, trace_dir, label):
+    """Clock, MFMA busy, VALU, LDS and L2 figures of the attention kernels (MI355X: 8 XCDs,
+    1024 SIMDs; GRBM_GUI_ACTIVE sums the XCDs)."""
+    def per_kernel(run_dir):
+        out = {}
+        for path in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as f:
+                for r in csv.DictReader(f):
+                    name = r["Kernel_Name"].split("(")[0].replace("void ", "").replace("psa::", "")
+                    if name.startswith(("psa_sparse", "psa_dense")):
+                        out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        return {k: {c: sum(v) / len(v) for c, v in d.items()} for k, d in out.items()}
+    sq, tcc = per_kernel(sq_dir), per_kernel(tcc_dir)
+    dur = {}
+    for path in glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                dur[r["Name"].split("(")[0].replace("void ", "").replace("psa::", "")] = float(r["AverageNs"]) * 1e-9
+    rows = []
+    for k in sorted(sq):
+        a, b, t = sq[k], tcc[k], dur[k]
+        cyc = a["GRBM_GUI_ACTIVE"] / 8.0
+        rows.append("| %s | %s | %.2f | %.2f | %.3f | %.1f | %.2f | %.3f | %.0f | %.3f |" % (
+            label, k, t * 1e3, cyc / t / 1e9, a["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * 1024),
+            a["SQ_VALU_MFMA_BUSY_CYCLES"] / a["SQ_INSTS_MFMA"], a["SQ_INSTS_VALU"] / a["SQ_INSTS_MFMA"],
+            a["SQ_ACTIVE_INST_VALU"] * 4 / (cyc * 1024), a["SQ_LDS_BANK_CONFLICT"],
+            b["TCC_HIT_sum"] / (b["TCC_HIT_sum"] + b["TCC_MISS_sum"])))
+    return rows
+
+
+UTIL_HEADER = ("| workload | kernel | ms (trace) | clock GHz | MFMA busy | MFMA cycles per MFMA | "
+               "VALU insts per MFMA | VALU active | LDS bank-conflict cycles | L2 hit |\n"
+               "|---|---|---|---|---|---|---|---|---|---|")
+
+
 def recorded_traffic():
     """Bytes per launch of the sparse kernel from the committed counter summary, or None when
     the summary is missing or the kernel sources changed since it was taken."""
@@ -246,6 +284,11 @@ def main():
     args = parse()
     if args.kernel_stats:
         sys.stdout.write(kernel_stats_table(args.kernel_stats))
+        return 0
+    if args.utilisation:
+        label = os.path.basename(os.path.normpath(args.utilisation[0]))
+        print(UTIL_HEADER)
+        print("\n".join(utilisation_rows(*args.utilisation, label)))
         return 0
     if args.counters:
         sys.stdout.write(summarise_counters(args.counters[0], args.counters[1], args.copy_calibration_mb))
