@@ -10,6 +10,9 @@ imports nothing from it.  Everything here is plain numpy, computed in float64:
 * ``attention`` -- naive masked softmax attention: exact softmax attention restricted to the
                    kept blocks, with padded keys excluded (Algorithm 2's consumer body computes
                    exactly this up to rounding).
+* ``psablock``  -- 3D PSABlocks with 3D padding (Sec. 3.2): the PSABlock grid, the group of
+                   every original token, Algorithm 1 on the PSABlock grid, and the
+                   PSABlock-centric (T', H', W', bt, bh, bw) layout.
 
 Every function is pinned by tests against values fixed by the paper and by mathematics
 (hand-worked maps, closed-form counts, symmetry and periodicity invariants, library softmax
@@ -18,3 +21,5 @@ attention, brute force on tiny inputs); see the ``tests/test_oracle_*.py`` files
 from .stripe import (STRIDE_INF, axis_condition, is_attending, block_coordinates,  # noqa: F401
                      blockmap, kept_per_row, kept_per_head)
 from .attention import masked_attention  # noqa: F401
+from .psablock import (psablock_grid, token_groups, group_coordinates,  # noqa: F401
+                       psablock_map, to_blocks, from_blocks)

@@ -17,12 +17,15 @@ does not state it; the workloads use 1/sqrt(d)).  Arithmetic is float64 on the g
 import numpy as np
 
 
-def masked_attention(q, k, v, keep, block, scale, rows=None):
+def masked_attention(q, k, v, keep, block, scale, rows=None, groups=None):
     """Masked attention for one (batch, head).
 
     q, k, v : arrays [N, d] (any float dtype; upcast to float64)
     keep    : bool/uint8 array [nb, nb], row = query block, column = key block
+    block   : tokens per block (block b = tokens [b*block, (b+1)*block))
     rows    : query token indices to evaluate (default: all N)
+    groups  : optional int array [N], the block of every token when blocks are not runs of
+              consecutive tokens (PSABlocks of the original token order); `block` is then unused
     returns : (o [R, d] float64, lse [R] float64)
     """
     q = np.asarray(q, dtype=np.float64)
@@ -31,8 +34,8 @@ def masked_attention(q, k, v, keep, block, scale, rows=None):
     keep = np.asarray(keep).astype(bool)
     n = k.shape[0]
     rows = np.arange(n) if rows is None else np.asarray(rows, dtype=np.int64)
-    key_block = np.arange(n) // block
-    mask = keep[rows // block][:, key_block]                 # [R, N]: q_i may attend to k_j
+    key_block = np.arange(n) // block if groups is None else np.asarray(groups, dtype=np.int64)
+    mask = keep[key_block[rows]][:, key_block]               # [R, N]: q_i may attend to k_j
     s = scale * (q[rows] @ k.T)
     s = np.where(mask, s, -np.inf)
     m = s.max(axis=1)

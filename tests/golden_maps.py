@@ -1,15 +1,17 @@
-"""Reader for tests/golden/stripe_maps.txt (hand-worked block maps)."""
+"""Reader for the hand-worked map files under tests/golden/ (stripe_maps.txt: one-dimensional
+blocks; psablock_maps.txt: 3D PSABlocks)."""
 import os
 
 import numpy as np
 
 INF = 2 ** 31 - 1
 PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "stripe_maps.txt")
+PSABLOCK_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "psablock_maps.txt")
 
 
-def load():
+def load(path=PATH):
     cases, cur, in_map = [], None, False
-    with open(PATH) as f:
+    with open(path) as f:
         for raw in f:
             line = raw.strip()
             if not line or line.startswith("#"):
@@ -26,6 +28,8 @@ def load():
             key, _, val = (x.strip() for x in line.partition("="))
             if key == "grid":
                 cur["grid"] = tuple(int(x) for x in val.split())
+            elif key == "pb":
+                cur["pb"] = tuple(int(x) for x in val.split())
             elif key == "m":
                 cur["m"] = tuple(INF if x == "inf" else int(x) for x in val.split())
             elif key == "kept":
