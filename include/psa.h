@@ -155,6 +155,71 @@ psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o,
                            int32_t n_heads, int32_t head_dim, int32_t n_tokens, int32_t block,
                            float softmax_scale, float* lse, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------------------------
+ * 3D PSABlocks and 3D padding (Sec. 3.2, "Hardware-Aware Design" and "3D-Padding for Resolution
+ * Flexibility").  A PSABlock is a bt x bh x bw tile of the F x H x W video grid; each axis is
+ * padded to the smallest multiple of its block size, giving a grid of PSABlocks
+ * T' = ceil(F / bt), H' = ceil(H / bh), W' = ceil(W / bw).  Algorithm 1 runs on that grid: a
+ * PSABlock (t', h', w') has temporal coordinate t' and spatial coordinate h' W' + w', so
+ * temporal parameters count PSABlocks along time and spatial parameters count PSABlocks of the
+ * H' x W' plane.  Text tokens (after the video) are global.
+ *
+ * The PSABlock-centric layout of a [batch*heads][F*H*W + n_text][head_dim] tensor is
+ * [batch*heads][T' H' W' bt bh bw + n_text][head_dim]: PSABlocks in row-major (t', h', w')
+ * order, the tokens of each PSABlock contiguous in row-major (t, h, w) order, zeros at padded
+ * positions, then the text tokens.  Attention runs on that layout in tiles of 64 or 128
+ * positions (a PSABlock must be a whole number of tiles); padded keys get -inf before the
+ * softmax (Algorithm 2), a tile holding only padding is never visited, and O rows at padded
+ * positions are unspecified (psa_from_blocks drops them).
+ * --------------------------------------------------------------------------------------------- */
+
+/* PSABlock shape (bt, bh, bw), each >= 1. */
+typedef struct {
+  int32_t t, h, w;
+} psa_block3d_t;
+
+/* Positions of the PSABlock-centric layout, T' H' W' bt bh bw + n_text, or -1 if invalid. */
+int64_t psa_blocked_tokens(psa_grid_t grid, psa_block3d_t pb);
+
+/* Original -> PSABlock-centric layout (and back: psa_from_blocks, which drops padded rows).
+ *   x   device bf16 [batch_heads][F*H*W + n_text][head_dim]
+ *   xb  device bf16 [batch_heads][psa_blocked_tokens(grid, pb)][head_dim]
+ * head_dim 64 or 128, batch_heads <= 65535.  Memory-bound copies; source and destination
+ * must not overlap. */
+psa_status_t psa_to_blocks(const void* x, void* xb, int32_t batch_heads, int32_t head_dim,
+                           psa_grid_t grid, psa_block3d_t pb, hipStream_t stream);
+psa_status_t psa_from_blocks(const void* xb, void* x, int32_t batch_heads, int32_t head_dim,
+                             psa_grid_t grid, psa_block3d_t pb, hipStream_t stream);
+
+/* Block map of Algorithm 1 at PSABlock granularity.  G = T'H'W' groups (+1: the text, last):
+ *   blockmap device uint8 [n_heads][G][G], kept_per_row int32 [n_heads][G],
+ *   kept_per_head int64 [n_heads]; any may be NULL. */
+psa_status_t psa_build_blockmap_3d(const psa_stripe_t* params, int32_t n_heads, psa_grid_t grid,
+                                   psa_block3d_t pb, uint8_t* blockmap, int32_t* kept_per_row,
+                                   int64_t* kept_per_head, hipStream_t stream);
+
+/* Workspace bytes of psa_attention_plan_3d / psa_attention_run_3d (0 if invalid); it also holds
+ * the valid positions of every tile (16 bytes per tile). */
+size_t psa_workspace_size_3d(int32_t batch, int32_t n_heads, psa_grid_t grid, psa_block3d_t pb,
+                             int32_t tile);
+
+/* Plan of the sparse attention over the PSABlock-centric layout, as psa_attention_plan.  The
+ * work items are the tiles; kept_per_tile (device int32 [n_heads][nt], nt = ceil(
+ * psa_blocked_tokens / tile), or NULL) receives the kept key tiles of every query tile (0 for a
+ * tile of padding).  Limits: nt <= PSA_MAX_BLOCKS, batch * n_heads <= PSA_MAX_BATCH_HEADS. */
+psa_status_t psa_attention_plan_3d(int32_t batch, int32_t n_heads, psa_grid_t grid,
+                                   psa_block3d_t pb, int32_t tile, const psa_stripe_t* params,
+                                   void* workspace, size_t workspace_bytes,
+                                   int32_t* kept_per_tile, hipStream_t stream);
+
+/* Sparse attention over a 3D plan, as psa_attention_run; q, k, v, o (and lse: fp32
+ * [batch][n_heads][psa_blocked_tokens]) are in the PSABlock-centric layout. */
+psa_status_t psa_attention_run_3d(const void* q, const void* k, const void* v, void* o,
+                                  int32_t batch, int32_t n_heads, int32_t head_dim,
+                                  psa_grid_t grid, psa_block3d_t pb, int32_t tile,
+                                  float softmax_scale, void* workspace, size_t workspace_bytes,
+                                  float* lse, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* psa_status_string(psa_status_t status);
 

@@ -11,6 +11,13 @@ is no CPU or PyTorch fallback.
     ws = plan(params, grid, block, batch=1)                   # plan once ...
     o = run(q, k, v, grid, block, ws)                         # ... run many times
     bmap, per_row, per_head = build_blockmap(params, (F, H, W, n_text), block=128)
+
+3D PSABlocks with 3D padding (the paper's layout; q, k, v permuted once, e.g. for a whole DiT):
+
+    pb = (3, 8, 16)
+    qb, kb, vb = (to_blocks(x, grid, pb) for x in (q, k, v))
+    ob = attention_fwd_3d(qb, kb, vb, grid, pb, params, tile=128)
+    o = from_blocks(ob, grid, pb)
 """
 import math
 
@@ -18,7 +25,9 @@ from . import _lib
 from ._lib import STRIDE_INF, PsaError  # noqa: F401
 
 __all__ = ["STRIDE_INF", "PsaError", "num_blocks", "workspace_size", "build_blockmap",
-           "attention_fwd", "plan", "run", "dense_fwd", "Workspace", "library_path"]
+           "attention_fwd", "plan", "run", "dense_fwd", "Workspace", "library_path",
+           "blocked_tokens", "to_blocks", "from_blocks", "build_blockmap_3d", "plan_3d", "run_3d",
+           "attention_fwd_3d"]
 
 
 def library_path():
@@ -207,3 +216,130 @@ def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=Non
         _lib.check(_lib.lib().psa_dense_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, n, int(block),
                                             scale, _ptr(lse), _stream(stream, q.device)))
     return (o, lse) if return_lse else o
+
+
+# ---------------------------------------------------------------------------------------------
+# 3D PSABlocks with 3D padding (include/psa.h, second part).
+# ---------------------------------------------------------------------------------------------
+
+def blocked_tokens(grid, pb):
+    """Positions of the PSABlock-centric layout (T' H' W' bt bh bw + n_text)."""
+    return int(_lib.lib().psa_blocked_tokens(_grid(grid), _lib.block3d_of(pb)))
+
+
+def _layout(src, grid, pb, out, stream, to):
+    torch = _torch()
+    if src.dtype != torch.bfloat16 or not src.is_cuda or not src.is_contiguous() or src.dim() != 4:
+        raise ValueError("expected a contiguous bf16 GPU tensor [batch, heads, tokens, head_dim]")
+    b, h, n, d = src.shape
+    g = _grid_tuple(grid)
+    n_orig = g[0] * g[1] * g[2] + g[3]
+    n_blk = blocked_tokens(grid, pb)
+    if n_blk < 0:
+        raise ValueError("invalid grid or PSABlock shape")
+    if n != (n_orig if to else n_blk):
+        raise ValueError("tensor has %d tokens, the %s layout has %d" % (n, "original" if to else "blocked",
+                                                                        n_orig if to else n_blk))
+    shape = (b, h, n_blk if to else n_orig, d)
+    dst = torch.empty(shape, dtype=src.dtype, device=src.device) if out is None else out
+    if tuple(dst.shape) != shape or not dst.is_contiguous() or dst.dtype != src.dtype:
+        raise ValueError("out must be a contiguous bf16 tensor of shape %s" % (shape,))
+    fn = _lib.lib().psa_to_blocks if to else _lib.lib().psa_from_blocks
+    with torch.cuda.device(src.device):
+        _lib.check(fn(_ptr(src), _ptr(dst), b * h, d, _grid(grid), _lib.block3d_of(pb),
+                      _stream(stream, src.device)))
+    return dst
+
+
+def to_blocks(x, grid, pb, out=None, stream=None):
+    """[batch, heads, F*H*W + n_text, d] -> PSABlock-centric layout (psa_to_blocks)."""
+    return _layout(x, grid, pb, out, stream, True)
+
+
+def from_blocks(xb, grid, pb, out=None, stream=None):
+    """PSABlock-centric layout -> [batch, heads, F*H*W + n_text, d] (psa_from_blocks)."""
+    return _layout(xb, grid, pb, out, stream, False)
+
+
+def build_blockmap_3d(params, grid, pb, device=None, blockmap=True, per_row=True, per_head=True,
+                      stream=None):
+    """PSABlock-level map: (uint8 [heads, G, G] | None, int32 [heads, G] | None,
+    int64 [heads] | None), G = T'H'W' (+1 for the text group)."""
+    torch = _torch()
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    g = _grid_tuple(grid)
+    (tp, hp, wp) = (-(-g[0] // pb[0]), -(-g[1] // pb[1]), -(-g[2] // pb[2]))
+    groups = tp * hp * wp + (1 if g[3] > 0 else 0)
+    heads = len(params)
+    bm = torch.empty((heads, groups, groups), dtype=torch.uint8, device=device) if blockmap else None
+    pr = torch.empty((heads, groups), dtype=torch.int32, device=device) if per_row else None
+    ph = torch.empty((heads,), dtype=torch.int64, device=device) if per_head else None
+    with torch.cuda.device(device):
+        _lib.check(_lib.lib().psa_build_blockmap_3d(_lib.stripes(params), heads, _grid(grid),
+                                                    _lib.block3d_of(pb), _ptr(bm), _ptr(pr), _ptr(ph),
+                                                    _stream(stream, device)))
+    return bm, pr, ph
+
+
+class Workspace3d(Workspace):
+    """Workspace of plan_3d / run_3d."""
+
+    def __init__(self, batch, n_heads, grid, pb, tile, device):
+        torch = _torch()
+        self.nbytes = int(_lib.lib().psa_workspace_size_3d(int(batch), int(n_heads), _grid(grid),
+                                                            _lib.block3d_of(pb), int(tile)))
+        if self.nbytes == 0:
+            raise ValueError("invalid sizes for a 3D workspace")
+        self.tensor = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+        self.sizes = (int(batch), int(n_heads), _grid_tuple(grid), tuple(int(x) for x in pb), int(tile))
+        self.params = None
+
+
+def plan_3d(params, grid, pb, tile=128, batch=1, device=None, workspace=None,
+            return_kept_per_tile=False, stream=None):
+    """Plan over the PSABlock-centric layout (psa_attention_plan_3d)."""
+    torch = _torch()
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    h = len(params)
+    ws = workspace if workspace is not None else Workspace3d(batch, h, grid, pb, tile, device)
+    n_tiles = -(-blocked_tokens(grid, pb) // int(tile))
+    kept = torch.empty((h, n_tiles), dtype=torch.int32, device=device) if return_kept_per_tile else None
+    with torch.cuda.device(device):
+        _lib.check(_lib.lib().psa_attention_plan_3d(int(batch), h, _grid(grid), _lib.block3d_of(pb),
+                                                    int(tile), _lib.stripes(params), _ptr(ws.tensor),
+                                                    ws.nbytes, _ptr(kept), _stream(stream, device)))
+    ws.sizes = (int(batch), h, _grid_tuple(grid), tuple(int(x) for x in pb), int(tile))
+    ws.params = [tuple(int(x) for x in m) for m in params]
+    return (ws, kept) if return_kept_per_tile else ws
+
+
+def run_3d(q, k, v, grid, pb, tile, workspace, scale=None, out=None, return_lse=False, stream=None):
+    """Sparse attention over a 3D plan; q, k, v, o in the PSABlock-centric layout."""
+    torch = _torch()
+    _check_qkv(q, k, v)
+    b, h, n, d = q.shape
+    if n != blocked_tokens(grid, pb):
+        raise ValueError("q, k, v must be in the PSABlock-centric layout (%d tokens)" % blocked_tokens(grid, pb))
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q) if out is None else out
+    _check_qkv(q, o)
+    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+    ws = workspace
+    if ws.params is None:
+        raise ValueError("the workspace holds no plan: call plan_3d() first")
+    if ws.sizes != (b, h, _grid_tuple(grid), tuple(int(x) for x in pb), int(tile)):
+        raise ValueError("the workspace was planned for %s, not %s"
+                         % (ws.sizes, (b, h, _grid_tuple(grid), tuple(pb), int(tile))))
+    with torch.cuda.device(q.device):
+        _lib.check(_lib.lib().psa_attention_run_3d(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, _grid(grid), _lib.block3d_of(pb), int(tile),
+            scale, _ptr(ws.tensor), ws.nbytes, _ptr(lse), _stream(stream, q.device)))
+    return (o, lse) if return_lse else o
+
+
+def attention_fwd_3d(q, k, v, grid, pb, params, tile=128, scale=None, out=None, return_lse=False,
+                     workspace=None, stream=None):
+    """plan_3d then run_3d (q, k, v in the PSABlock-centric layout)."""
+    b = q.shape[0]
+    ws = plan_3d(params, grid, pb, tile, batch=b, device=q.device, workspace=workspace, stream=stream)
+    return run_3d(q, k, v, grid, pb, tile, ws, scale, out, return_lse, stream)

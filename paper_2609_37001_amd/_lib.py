@@ -22,8 +22,9 @@ PSA_ERR_WORKSPACE = 3
 PSA_ERR_HIP = 4
 
 EXPORTS = ("psa_num_blocks", "psa_workspace_size", "psa_build_blockmap", "psa_attention_plan",
-           "psa_attention_run", "psa_attention_fwd", "psa_dense_fwd", "psa_status_string",
-           "psa_last_error")
+           "psa_attention_run", "psa_attention_fwd", "psa_dense_fwd", "psa_blocked_tokens",
+           "psa_to_blocks", "psa_from_blocks", "psa_build_blockmap_3d", "psa_workspace_size_3d",
+           "psa_attention_plan_3d", "psa_attention_run_3d", "psa_status_string", "psa_last_error")
 
 
 class Stripe(ctypes.Structure):
@@ -34,6 +35,10 @@ class Stripe(ctypes.Structure):
 class Grid(ctypes.Structure):
     _fields_ = [("frames", ctypes.c_int32), ("height", ctypes.c_int32),
                 ("width", ctypes.c_int32), ("n_text", ctypes.c_int32)]
+
+
+class Block3d(ctypes.Structure):
+    _fields_ = [("t", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32)]
 
 
 class PsaError(RuntimeError):
@@ -81,12 +86,26 @@ def lib():
         L.psa_attention_fwd.restype = ctypes.c_int
         L.psa_dense_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, vp, vp]
         L.psa_dense_fwd.restype = ctypes.c_int
+        L.psa_blocked_tokens.argtypes = [Grid, Block3d]
+        L.psa_blocked_tokens.restype = i64
+        for name in ("psa_to_blocks", "psa_from_blocks"):
+            getattr(L, name).argtypes = [vp, vp, i32, i32, Grid, Block3d, vp]
+            getattr(L, name).restype = ctypes.c_int
+        L.psa_build_blockmap_3d.argtypes = [ctypes.POINTER(Stripe), i32, Grid, Block3d, vp, vp, vp, vp]
+        L.psa_build_blockmap_3d.restype = ctypes.c_int
+        L.psa_workspace_size_3d.argtypes = [i32, i32, Grid, Block3d, i32]
+        L.psa_workspace_size_3d.restype = sz
+        L.psa_attention_plan_3d.argtypes = [i32, i32, Grid, Block3d, i32, ctypes.POINTER(Stripe), vp, sz,
+                                            vp, vp]
+        L.psa_attention_plan_3d.restype = ctypes.c_int
+        L.psa_attention_run_3d.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, Block3d, i32,
+                                           ctypes.c_float, vp, sz, vp, vp]
+        L.psa_attention_run_3d.restype = ctypes.c_int
         L.psa_status_string.argtypes = [ctypes.c_int]
         L.psa_status_string.restype = ctypes.c_char_p
         L.psa_last_error.argtypes = []
         L.psa_last_error.restype = ctypes.c_char_p
         _lib = L
-        del i64
     return _lib
 
 
@@ -106,3 +125,8 @@ def stripes(params):
 
 def grid_of(frames, height, width, n_text=0):
     return Grid(int(frames), int(height), int(width), int(n_text))
+
+
+def block3d_of(pb):
+    t, h, w = (int(x) for x in pb)
+    return Block3d(t, h, w)

@@ -64,7 +64,38 @@ __device__ __forceinline__ int2 block_coord(const Geometry& g, int32_t b) {
   return make_int2(t, (i0 - t * g.hw) / g.block);
 }
 
+// Coordinates of tile b of the PSABlock-centric layout: those of the PSABlock holding it
+// (t', s' = h' W' + w'), or global for a text tile.  A PSABlock is a whole number of tiles.
+__device__ __forceinline__ int2 tile_coord3d(const Geometry& g, int32_t b) {
+  const int32_t i0 = b * g.block;
+  if (i0 >= g.n_blk) return make_int2(-1, 0);
+  const int32_t pb = i0 / (g.pbt * g.pbh * g.pbw), plane = g.hp * g.wp;
+  const int32_t t = pb / plane;
+  return make_int2(t, pb - t * plane);
+}
+
+// Coordinates of group i of a PSABlock-level map: PSABlock i, or the text group (global).
+__device__ __forceinline__ int2 group_coord(const Geometry& g, int32_t i) {
+  const int32_t plane = g.hp * g.wp;
+  if (i >= g.tp * plane) return make_int2(-1, 0);
+  const int32_t t = i / plane;
+  return make_int2(t, i - t * plane);
+}
+
+// Whether position p of the PSABlock-centric layout holds a token (not 3D padding, not past
+// the end).
+__device__ __forceinline__ bool position_valid(const Geometry& g, int32_t p) {
+  if (p >= g.n) return false;
+  if (p >= g.n_blk) return true;
+  const int32_t area = g.pbh * g.pbw, vol = g.pbt * area, plane = g.hp * g.wp;
+  const int32_t pb = p / vol, x = p - pb * vol;
+  const int32_t tq = pb / plane, r = pb - tq * plane, hq = r / g.wp, wq = r - hq * g.wp;
+  const int32_t it = x / area, r2 = x - it * area, ih = r2 / g.pbw, iw = r2 - ih * g.pbw;
+  return tq * g.pbt + it < g.frames && hq * g.pbh + ih < g.height && wq * g.pbw + iw < g.width;
+}
+
 __device__ __forceinline__ bool tile_keep(const psa_stripe_t& m, int2 q, int2 k) {
+  if (q.x == kDeadTile || k.x == kDeadTile) return false;
   if (q.x < 0 || k.x < 0) return true;
   return axis_keep(k.x - q.x, m.t_w, m.t_o, m.t_s) && axis_keep(k.y - q.y, m.s_w, m.s_o, m.s_s);
 }
@@ -78,6 +109,13 @@ __device__ __forceinline__ int wave_sum(int v) {
 // Block map (psa_build_blockmap).
 // ---------------------------------------------------------------------------------------------
 
+// Coordinates of entry i of a block map: a one-dimensional block, or a PSABlock-level group.
+template <bool GROUPS>
+__device__ __forceinline__ int2 map_coord(const Geometry& g, int32_t i) {
+  return GROUPS ? group_coord(g, i) : block_coord(g, i);
+}
+
+template <bool GROUPS>
 __global__ __launch_bounds__(256) void psa_blockmap_kernel(ParamChunk pc, int32_t head0,
                                                            Geometry g, uint8_t* __restrict__ map) {
   const int32_t hc = blockIdx.y;
@@ -85,11 +123,12 @@ __global__ __launch_bounds__(256) void psa_blockmap_kernel(ParamChunk pc, int32_
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (p >= pairs) return;
   const int32_t qb = (int32_t)(p / g.nb), kb = (int32_t)(p - (int64_t)qb * g.nb);
-  const bool keep = tile_keep(pc.m[hc], block_coord(g, qb), block_coord(g, kb));
+  const bool keep = tile_keep(pc.m[hc], map_coord<GROUPS>(g, qb), map_coord<GROUPS>(g, kb));
   map[(int64_t)(head0 + hc) * pairs + p] = keep ? 1 : 0;
 }
 
 // One workgroup per head: per-row counts and the head total (deterministic, no atomics).
+template <bool GROUPS>
 __global__ __launch_bounds__(256) void psa_rowcount_kernel(ParamChunk pc, int32_t head0,
                                                            Geometry g,
                                                            int32_t* __restrict__ kept_per_row,
@@ -99,9 +138,10 @@ __global__ __launch_bounds__(256) void psa_rowcount_kernel(ParamChunk pc, int32_
   const psa_stripe_t m = pc.m[hc];
   int64_t total = 0;
   for (int32_t qb = wave; qb < g.nb; qb += 4) {
-    const int2 cq = block_coord(g, qb);
+    const int2 cq = map_coord<GROUPS>(g, qb);
     int cnt = 0;
-    for (int32_t kb = lane; kb < g.nb; kb += 64) cnt += tile_keep(m, cq, block_coord(g, kb)) ? 1 : 0;
+    for (int32_t kb = lane; kb < g.nb; kb += 64)
+      cnt += tile_keep(m, cq, map_coord<GROUPS>(g, kb)) ? 1 : 0;
     cnt = wave_sum(cnt);
     if (lane == 0 && kept_per_row) kept_per_row[(int64_t)(head0 + hc) * g.nb + qb] = cnt;
     total += cnt;
@@ -112,29 +152,108 @@ __global__ __launch_bounds__(256) void psa_rowcount_kernel(ParamChunk pc, int32_
     kept_per_head[head0 + hc] = partial[0] + partial[1] + partial[2] + partial[3];
 }
 
-hipError_t launch_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& g,
-                           uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
-                           hipStream_t stream) {
+template <bool GROUPS>
+static hipError_t launch_map(const ParamChunk& pc, int32_t head0, const Geometry& g,
+                             uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
+                             hipStream_t stream) {
   if (blockmap) {
     const int64_t pairs = (int64_t)g.nb * g.nb;
     dim3 grid((unsigned)((pairs + 255) / 256), (unsigned)pc.n);
-    hipLaunchKernelGGL(psa_blockmap_kernel, grid, dim3(256), 0, stream, pc, head0, g, blockmap);
+    hipLaunchKernelGGL(psa_blockmap_kernel<GROUPS>, grid, dim3(256), 0, stream, pc, head0, g, blockmap);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (kept_per_row || kept_per_head) {
-    hipLaunchKernelGGL(psa_rowcount_kernel, dim3(pc.n), dim3(256), 0, stream, pc, head0, g,
+    hipLaunchKernelGGL(psa_rowcount_kernel<GROUPS>, dim3(pc.n), dim3(256), 0, stream, pc, head0, g,
                        kept_per_row, kept_per_head);
     return hipGetLastError();
   }
   return hipSuccess;
 }
 
+hipError_t launch_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& g,
+                           uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
+                           hipStream_t stream) {
+  return launch_map<false>(pc, head0, g, blockmap, kept_per_row, kept_per_head, stream);
+}
+
+hipError_t launch_group_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& g,
+                                 uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
+                                 hipStream_t stream) {
+  return launch_map<true>(pc, head0, g, blockmap, kept_per_row, kept_per_head, stream);
+}
+
+// ---------------------------------------------------------------------------------------------
+// PSABlock-centric layout (psa_to_blocks / psa_from_blocks): one workgroup per (batch*head,
+// PSABlock), or per 64 text rows; 16-byte chunks, CPR per row.  The blocked side is written or
+// read in order, the original side in runs of bw rows.
+// ---------------------------------------------------------------------------------------------
+
+template <bool TO, int CPR>
+__global__ __launch_bounds__(256) void psa_layout_kernel(const uint4* __restrict__ src,
+                                                         uint4* __restrict__ dst, Geometry g) {
+  const int32_t n_p = g.tp * g.hp * g.wp;
+  const size_t n_orig = (size_t)g.n_video + g.n_text, n_blkd = (size_t)g.n;
+  const uint4* s = src + (size_t)blockIdx.y * (TO ? n_orig : n_blkd) * CPR;
+  uint4* d = dst + (size_t)blockIdx.y * (TO ? n_blkd : n_orig) * CPR;
+  if ((int32_t)blockIdx.x < n_p) {
+    const int32_t pb = blockIdx.x, plane = g.hp * g.wp, area = g.pbh * g.pbw;
+    const int32_t vol = g.pbt * area;
+    const int32_t tq = pb / plane, r = pb - tq * plane, hq = r / g.wp, wq = r - hq * g.wp;
+    const int32_t t0 = tq * g.pbt, h0 = hq * g.pbh, w0 = wq * g.pbw;
+    for (int32_t e = threadIdx.x; e < vol * CPR; e += 256) {
+      const int32_t x = e / CPR, c = e % CPR;
+      const int32_t it = x / area, r2 = x - it * area, ih = r2 / g.pbw, iw = r2 - ih * g.pbw;
+      const int32_t t = t0 + it, h = h0 + ih, w = w0 + iw;
+      const bool valid = t < g.frames && h < g.height && w < g.width;
+      const size_t orow = ((size_t)t * g.height + h) * g.width + w;
+      const size_t brow = (size_t)pb * vol + x;
+      if (TO)
+        d[brow * CPR + c] = valid ? s[orow * CPR + c] : make_uint4(0u, 0u, 0u, 0u);
+      else if (valid)
+        d[orow * CPR + c] = s[brow * CPR + c];
+    }
+  } else {
+    const int32_t r0 = ((int32_t)blockIdx.x - n_p) * 64;
+    for (int32_t e = threadIdx.x; e < 64 * CPR; e += 256) {
+      const int32_t rr = r0 + e / CPR, c = e % CPR;
+      if (rr < g.n_text) {
+        const size_t orow = (size_t)g.n_video + rr, brow = (size_t)g.n_blk + rr;
+        if (TO)
+          d[brow * CPR + c] = s[orow * CPR + c];
+        else
+          d[orow * CPR + c] = s[brow * CPR + c];
+      }
+    }
+  }
+}
+
+template <bool TO, int CPR>
+static hipError_t launch_layout_t(const void* src, void* dst, int32_t n_bh, const Geometry& g,
+                                  hipStream_t stream) {
+  const int32_t n_p = g.tp * g.hp * g.wp;
+  dim3 grid((unsigned)(n_p + (g.n_text + 63) / 64), (unsigned)n_bh);
+  hipLaunchKernelGGL((psa_layout_kernel<TO, CPR>), grid, dim3(256), 0, stream, (const uint4*)src,
+                     (uint4*)dst, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_layout(const void* src, void* dst, int32_t n_bh, int32_t head_dim,
+                         const Geometry& g, bool to_blocks, hipStream_t stream) {
+  if (head_dim == 128)
+    return to_blocks ? launch_layout_t<true, 16>(src, dst, n_bh, g, stream)
+                     : launch_layout_t<false, 16>(src, dst, n_bh, g, stream);
+  if (head_dim == 64)
+    return to_blocks ? launch_layout_t<true, 8>(src, dst, n_bh, g, stream)
+                     : launch_layout_t<false, 8>(src, dst, n_bh, g, stream);
+  return hipErrorInvalidValue;
+}
+
 // ---------------------------------------------------------------------------------------------
 // Scheduler pre-pass (psa_attention_fwd).
 // ---------------------------------------------------------------------------------------------
 
-WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb) {
+WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb, bool masks) {
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t items = (size_t)batch * n_heads * nb;
   WorkspaceLayout wl;
@@ -144,12 +263,14 @@ WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb) {
   wl.counts = up(wl.coords + sizeof(int2) * (size_t)nb);
   wl.order = up(wl.counts + sizeof(int32_t) * items);
   wl.queues = up(wl.order + sizeof(int32_t) * items);
-  wl.total = up(wl.queues + sizeof(int32_t) * kQueueWords);
+  wl.masks = up(wl.queues + sizeof(int32_t) * kQueueWords);
+  wl.total = masks ? up(wl.masks + 2 * sizeof(uint64_t) * (size_t)nb) : wl.masks;
   return wl;
 }
 
 // Copies one chunk of stripe parameters into the workspace; the first chunk also invalidates
-// the plan header and writes the block coordinate table.
+// the plan header (write_coords != 0) and writes the block coordinate table of one-dimensional
+// blocks (write_coords == 1; 3D tiles get theirs from psa_tiles3d_kernel).
 __global__ __launch_bounds__(256) void psa_setup_kernel(ParamChunk pc, int32_t head0, Geometry g,
                                                         PlanHeader* __restrict__ header,
                                                         psa_stripe_t* __restrict__ params,
@@ -158,17 +279,40 @@ __global__ __launch_bounds__(256) void psa_setup_kernel(ParamChunk pc, int32_t h
   const int32_t i = blockIdx.x * 256 + threadIdx.x;
   if (write_coords && i == 0) header->magic = 0;
   if (i < pc.n) params[head0 + i] = pc.m[i];
-  if (write_coords && i < g.nb) coords[i] = block_coord(g, i);
+  if (write_coords == 1 && i < g.nb) coords[i] = block_coord(g, i);
+}
+
+// One wave per tile of the PSABlock-centric layout: the valid positions of the tile (bit r of
+// word r / 64) and its coordinates, kDeadTile when it holds only padding.
+__global__ __launch_bounds__(256) void psa_tiles3d_kernel(Geometry g, int2* __restrict__ coords,
+                                                          uint64_t* __restrict__ masks) {
+  const int32_t b = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (b >= g.nb) return;
+  const int32_t i0 = b * g.block;
+  const uint64_t lo = __builtin_amdgcn_ballot_w64(lane < g.block && position_valid(g, i0 + lane));
+  const uint64_t hi = g.block > 64 ? __builtin_amdgcn_ballot_w64(position_valid(g, i0 + 64 + lane))
+                                   : ~0ull;
+  if (lane == 0) {
+    masks[2 * b] = lo;
+    masks[2 * b + 1] = hi;
+    const bool dead = lo == 0 && (g.block <= 64 || hi == 0);
+    coords[b] = dead ? make_int2(kDeadTile, 0) : tile_coord3d(g, b);
+  }
 }
 
 hipError_t launch_setup(const ParamChunk& pc, int32_t head0, const Geometry& g, void* workspace,
                         const WorkspaceLayout& wl, bool write_coords, hipStream_t stream) {
   char* ws = (char*)workspace;
-  const int32_t n = write_coords ? max(g.nb, pc.n) : pc.n;
+  const bool blocks3d = g.pbt > 0;
+  const bool coords1d = write_coords && !blocks3d;
+  const int32_t n = coords1d ? max(g.nb, pc.n) : pc.n;
   hipLaunchKernelGGL(psa_setup_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, pc, head0, g,
                      (PlanHeader*)(ws + wl.header), (psa_stripe_t*)(ws + wl.params),
-                     (int2*)(ws + wl.coords),
-                     (int32_t)(write_coords ? 1 : 0));
+                     (int2*)(ws + wl.coords), (int32_t)(write_coords ? (coords1d ? 1 : 2) : 0));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !write_coords || !blocks3d) return e;
+  hipLaunchKernelGGL(psa_tiles3d_kernel, dim3((g.nb + 3) / 4), dim3(256), 0, stream, g,
+                     (int2*)(ws + wl.coords), (uint64_t*)(ws + wl.masks));
   return hipGetLastError();
 }
 
@@ -304,8 +448,13 @@ static PlanHeader plan_header(const Geometry& g, int32_t batch, int32_t n_heads)
   h.nb = g.nb;
   h.block = g.block;
   h.n = g.n;
-  h.hw = g.hw;
+  h.frames = g.frames;
+  h.height = g.height;
+  h.width = g.width;
   h.n_text = g.n_text;
+  h.pbt = g.pbt;
+  h.pbh = g.pbh;
+  h.pbw = g.pbw;
   return h;
 }
 
@@ -496,22 +645,37 @@ __device__ __forceinline__ void qk_half(const WaveState<D, BLK>& st,
 //    of 16-key chunk j.
 //  * V^T operand: within each 16-lane group, source lane 4r+c reads V[key0 + r][d0 + 4c .. +3];
 //    the transpose read hands lane i the four keys key0..key0+3 at head-dim d0 + i.
-template <int D, int BLK>
+//  * Masked keys: past the sequence end (one-dimensional blocks: only the last block), or, in
+//    the PSABlock-centric layout (PAD), every position whose bit in the tile's validity words
+//    (lo: positions 0..63, hi: 64..127) is clear -- 3D padding and the end of the sequence.
+template <int D, int BLK, bool PAD>
 __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
                                                 f32x16 (&s)[Half<D, BLK>::KT], const uint8_t* sv,
-                                                int kb, int k0, int n, bool tail,
-                                                int lane) {
+                                                int kb, int k0, int n, bool tail, uint64_t lo,
+                                                uint64_t hi, int lane) {
   using T = Tile<D, BLK>;
   using H = Half<D, BLK>;
   const int h = lane >> 5, g = lane >> 4, j16 = lane & 15;
   if (tail) {
-    asm volatile("" ::: "memory");        // keep the mask a branch taken once per item
-    const int kbase = kb * BLK + k0 + 8 * h;
+    asm volatile("" ::: "memory");        // keep the mask a branch taken only by partial tiles
+    if constexpr (PAD) {
 #pragma unroll
-    for (int kt = 0; kt < H::KT; kt++)
+      for (int kt = 0; kt < H::KT; kt++) {
+        // This lane's keys of group kt are positions r0 + {0..7, 16..23}: one 64-bit word.
+        const int r0 = k0 + 32 * kt + 8 * h;
+        const uint32_t win = (uint32_t)((r0 < 64 ? lo : hi) >> (r0 & 63));
 #pragma unroll
-      for (int i = 0; i < 16; i++)
-        if (kbase + kt * 32 + 16 * (i >> 3) + (i & 7) >= n) s[kt][i] = -__builtin_inff();
+        for (int i = 0; i < 16; i++)
+          if (!((win >> (16 * (i >> 3) + (i & 7))) & 1u)) s[kt][i] = -__builtin_inff();
+      }
+    } else {
+      const int kbase = kb * BLK + k0 + 8 * h;
+#pragma unroll
+      for (int kt = 0; kt < H::KT; kt++)
+#pragma unroll
+        for (int i = 0; i < 16; i++)
+          if (kbase + kt * 32 + 16 * (i >> 3) + (i & 7) >= n) s[kt][i] = -__builtin_inff();
+    }
   }
 
   // s holds S - base with base = -negm (the running max, or 0 before the first kept key).
@@ -572,37 +736,48 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
 //   softmax+PV(hi) | wait K(i+1), barrier, load V(i+1)
 // K(i+1) streams in during the second half of block i, V(i+1) during QK(lo) of block i+1; the
 // other workgroup on the CU covers the rest of the load latency.
-template <int D, int BLK>
+template <int D, int BLK, bool PAD>
 __device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<D, BLK>& plan,
                                            const __bf16* kh, const __bf16* vh, int kb, int kb_next,
                                            int n, const uint8_t* sk, const uint8_t* sv,
-                                           int lane) {
-  const bool tail = (kb + 1) * BLK > n;
+                                           const uint64_t* masks, int lane) {
+  uint64_t lo = ~0ull, hi = ~0ull;
+  bool tail;
+  if constexpr (PAD) {
+    const int kbu = __builtin_amdgcn_readfirstlane(kb);
+    lo = masks[2 * kbu];
+    hi = masks[2 * kbu + 1];
+    tail = (lo & hi) != ~0ull;
+  } else {
+    tail = (kb + 1) * BLK > n;
+  }
   using H = Half<D, BLK>;
   f32x16 s[H::KT];
   qk_half<D, BLK>(st, s, sk, 0, lane);
   wait_dma<0>();
   __syncthreads();
-  softmax_pv_half<D, BLK>(st, s, sv, kb, 0, n, tail, lane);
+  softmax_pv_half<D, BLK, PAD>(st, s, sv, kb, 0, n, tail, lo, hi, lane);
   qk_half<D, BLK>(st, s, sk, H::HK, lane);
   __syncthreads();
   if (kb_next >= 0) issue_block<D, BLK>(plan, kh, plan.lds_k, kb_next, n);
-  softmax_pv_half<D, BLK>(st, s, sv, kb, H::HK, n, tail, lane);
+  softmax_pv_half<D, BLK, PAD>(st, s, sv, kb, H::HK, n, tail, lo, hi, lane);
   wait_dma<0>();
   __syncthreads();
   if (kb_next >= 0) issue_block<D, BLK>(plan, vh, plan.lds_v, kb_next, n);
 }
 
 // One work item: query block qb of one (batch, head).  `list` holds the kept key blocks in
-// ascending order (SPARSE) or is ignored (dense: every block 0..nkv-1).
-template <int D, int BLK, bool SPARSE>
+// ascending order (SPARSE) or is ignored (dense: every block 0..nkv-1).  PAD: the sequence is
+// the PSABlock-centric layout and `masks` holds the valid positions of every tile.
+template <int D, int BLK, bool SPARSE, bool PAD = false>
 __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
                                              const __bf16* __restrict__ qh,
                                              const __bf16* __restrict__ kh,
                                              const __bf16* __restrict__ vh,
                                              __bf16* __restrict__ oh, float* __restrict__ lseh,
                                              int n, int qb, int nkv, const uint16_t* list,
-                                             float c, const uint8_t* sk, const uint8_t* sv) {
+                                             float c, const uint8_t* sk, const uint8_t* sv,
+                                             const uint64_t* masks = nullptr) {
   using T = Tile<D, BLK>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, r32 = lane & 31;
@@ -640,7 +815,7 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
   for (int it = 0; it < nkv; it++) {
     const int kb = kv(it);
     const int kb_next = it + 1 < nkv ? kv(it + 1) : -1;
-    block_step<D, BLK>(st, plan, kh, vh, kb, kb_next, n, sk, sv, lane);
+    block_step<D, BLK, PAD>(st, plan, kh, vh, kb, kb_next, n, sk, sv, masks, lane);
   }
 
   // Epilogue: O = O^T / l, rows past the end are not stored.
@@ -665,13 +840,13 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
 // Persistent sparse attention (two 4-wave workgroups per CU).  Workgroup w starts on queue w % kNumQueues (its XCD under
 // round-robin dispatch) and moves on to the next queue when one runs dry, so every workgroup
 // exits once all queues are exhausted.
-template <int D, int BLK>
+template <int D, int BLK, bool PAD>
 __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void psa_sparse_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     __bf16* __restrict__ o, float* __restrict__ lse, const psa_stripe_t* __restrict__ params,
     const int2* __restrict__ coords, const int32_t* __restrict__ order,
-    int32_t* __restrict__ queues, const PlanHeader* __restrict__ header, PlanHeader expect,
-    float c) {
+    int32_t* __restrict__ queues, const uint64_t* __restrict__ masks,
+    const PlanHeader* __restrict__ header, PlanHeader expect, float c) {
   using T = Tile<D, BLK>;
   __shared__ __attribute__((aligned(1024))) uint8_t sk[T::BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sv[T::BYTES];
@@ -682,8 +857,10 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
   // through its queues and no output is written.
   const PlanHeader h = *header;
   if (h.magic != kPlanMagic || h.n_bh != expect.n_bh || h.n_heads != expect.n_heads ||
-      h.nb != expect.nb || h.block != expect.block || h.n != expect.n || h.hw != expect.hw ||
-      h.n_text != expect.n_text)
+      h.nb != expect.nb || h.block != expect.block || h.n != expect.n ||
+      h.frames != expect.frames || h.height != expect.height || h.width != expect.width ||
+      h.n_text != expect.n_text || h.pbt != expect.pbt || h.pbh != expect.pbh ||
+      h.pbw != expect.pbw)
     return;
   const int32_t n_heads = expect.n_heads, n = expect.n, nb = expect.nb;
 
@@ -746,8 +923,9 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
 
     const size_t off = (size_t)bh * n * D;
-    process_item<D, BLK, true>(plan, q + off, k + off, v + off, o + off,
-                               lse ? lse + (size_t)bh * n : nullptr, n, qb, nkv, list, c, sk, sv);
+    process_item<D, BLK, true, PAD>(plan, q + off, k + off, v + off, o + off,
+                                    lse ? lse + (size_t)bh * n : nullptr, n, qb, nkv, list, c, sk,
+                                    sv, masks);
   }
 }
 
@@ -775,16 +953,17 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
                               lse ? lse + (size_t)bh * n : nullptr, n, qb, nb, nullptr, c, sk, sv);
 }
 
-template <int D, int BLK>
+template <int D, int BLK, bool PAD>
 static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, void* o,
                                   float* lse, const PlanHeader& expect, float c,
                                   void* workspace, const WorkspaceLayout& wl, int32_t n_wg,
                                   hipStream_t stream) {
   char* ws = (char*)workspace;
-  hipLaunchKernelGGL((psa_sparse_kernel<D, BLK>), dim3(n_wg), dim3(Tile<D, BLK>::kThreads), 0, stream,
+  hipLaunchKernelGGL((psa_sparse_kernel<D, BLK, PAD>), dim3(n_wg), dim3(Tile<D, BLK>::kThreads), 0, stream,
                      (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
                      (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
                      (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues),
+                     PAD ? (const uint64_t*)(ws + wl.masks) : nullptr,
                      (const PlanHeader*)(ws + wl.header), expect, c);
   return hipGetLastError();
 }
@@ -794,14 +973,25 @@ hipError_t launch_sparse(const void* q, const void* k, const void* v, void* o, f
                          float c, void* workspace, const WorkspaceLayout& wl, int32_t n_wg,
                          hipStream_t stream) {
   const PlanHeader e = plan_header(g, batch, n_heads);
+  if (g.pbt > 0) {
+    if (head_dim == 128 && g.block == 128)
+      return launch_sparse_t<128, 128, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    if (head_dim == 64 && g.block == 64)
+      return launch_sparse_t<64, 64, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    if (head_dim == 128 && g.block == 64)
+      return launch_sparse_t<128, 64, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    if (head_dim == 64 && g.block == 128)
+      return launch_sparse_t<64, 128, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return hipErrorInvalidValue;
+  }
   if (head_dim == 128 && g.block == 128)
-    return launch_sparse_t<128, 128>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<128, 128, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
   if (head_dim == 64 && g.block == 64)
-    return launch_sparse_t<64, 64>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<64, 64, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
   if (head_dim == 128 && g.block == 64)
-    return launch_sparse_t<128, 64>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<128, 64, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
   if (head_dim == 64 && g.block == 128)
-    return launch_sparse_t<64, 128>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<64, 128, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
   return hipErrorInvalidValue;
 }
 

@@ -21,28 +21,39 @@ struct ParamChunk {
   psa_stripe_t m[kHeadsPerChunk];
 };
 
-// Sequence geometry in blocks.
+// Sequence geometry in blocks.  With one-dimensional blocks (pbt = 0) a block is `block`
+// consecutive tokens of the frame-major sequence.  With 3D PSABlocks (pbt > 0) the sequence is
+// the PSABlock-centric layout: the padded grid ordered (T', H', W', bt, bh, bw), then the text
+// tokens; a block (tile) is `block` consecutive positions of it, and a PSABlock is a whole
+// number of tiles.
 struct Geometry {
-  int32_t hw;       // tokens per frame, H*W
+  int32_t hw;       // tokens per frame of the video grid, H*W
   int32_t n_video;  // F*H*W
-  int32_t n;        // n_video + n_text
+  int32_t n;        // tokens of the sequence: n_video + n_text, or n_blk + n_text (3D)
   int32_t n_text;
   int32_t block;
   int32_t nb;       // ceil(n / block)
+  int32_t frames, height, width;
+  int32_t pbt, pbh, pbw;   // PSABlock shape; pbt = 0 for one-dimensional blocks
+  int32_t tp, hp, wp;      // PSABlock grid T', H', W' (3D)
+  int32_t n_blk;           // positions of the padded video grid, T'H'W' * pbt*pbh*pbw (3D)
 };
+
+// Coordinate of a tile that holds only padding: never kept as a key, no work as a query.
+constexpr int32_t kDeadTile = -2;
 
 // Identifies a finished plan in the workspace header; the sizes it was made for follow it.
 constexpr uint32_t kPlanMagic = 0x50534131u;  // "PSA1"
 
 struct PlanHeader {
-  uint32_t magic;   // kPlanMagic once psa_attention_plan's kernels have run, 0 while they run
+  uint32_t magic;   // kPlanMagic once the plan's kernels have run, 0 while they run
   int32_t n_bh;     // batch * n_heads
   int32_t n_heads;
   int32_t nb;
   int32_t block;
   int32_t n;
-  int32_t hw;
-  int32_t n_text;
+  int32_t frames, height, width, n_text;
+  int32_t pbt, pbh, pbw;
 };
 
 // Layout of the queue area: kNumQueues + 1 boundaries, kNumQueues pop counters, one exit
@@ -59,10 +70,11 @@ struct WorkspaceLayout {
   size_t counts;    // int32 [batch*n_heads*nb]: kept key blocks per work item
   size_t order;     // int32 [batch*n_heads*nb]: work items in schedule order
   size_t queues;    // int32 [kQueueWords]: queue boundaries, pop counters, exit counter
+  size_t masks;     // uint64 [nb][2]: valid positions of each tile (3D only)
   size_t total;
 };
 
-WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb);
+WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb, bool masks);
 
 // Launchers; each returns the hipError_t of its launch(es).
 hipError_t launch_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& g,
@@ -71,6 +83,16 @@ hipError_t launch_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& 
 
 hipError_t launch_setup(const ParamChunk& pc, int32_t head0, const Geometry& g, void* workspace,
                         const WorkspaceLayout& wl, bool write_coords, hipStream_t stream);
+
+// PSABlock-level block map: groups 0 .. T'H'W'-1 are the PSABlocks, group T'H'W' (with text)
+// the text; g.nb must be the group count.
+hipError_t launch_group_blockmap(const ParamChunk& pc, int32_t head0, const Geometry& g,
+                                 uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
+                                 hipStream_t stream);
+
+// PSABlock-centric layout of [bh][tokens][d] tensors (to: original -> blocked, else back).
+hipError_t launch_layout(const void* src, void* dst, int32_t n_bh, int32_t head_dim,
+                         const Geometry& g, bool to_blocks, hipStream_t stream);
 
 // Counts the kept blocks of every work item, orders them, and writes the header last.
 hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, void* workspace,

@@ -15,7 +15,7 @@ INF = _lib.STRIDE_INF
 
 def header_functions():
     text = open(os.path.join(ROOT, "include", "psa.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:const char\*|int32_t|size_t|psa_status_t)\s+(psa_\w+)\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:const char\*|int32_t|int64_t|size_t|psa_status_t)\s+(psa_\w+)\(", text, re.M)))
 
 
 def test_header_declares_the_boundary():
@@ -136,3 +136,63 @@ def test_run_validation_codes():
     assert _run(ws=0) == _lib.PSA_ERR_WORKSPACE
     assert _run(wsb=100) == _lib.PSA_ERR_WORKSPACE
 
+
+
+def _b3(t, h, w):
+    return _lib.block3d_of((t, h, w))
+
+
+def test_blocked_tokens_and_3d_workspace():
+    L = _lib.lib()
+    assert L.psa_blocked_tokens(_lib.grid_of(21, 45, 80), _b3(3, 8, 16)) == 21 * 48 * 80
+    assert L.psa_blocked_tokens(_lib.grid_of(33, 45, 80, 256), _b3(3, 8, 16)) == 33 * 48 * 80 + 256
+    assert L.psa_blocked_tokens(_lib.grid_of(30, 48, 80), _b3(6, 8, 8)) == 30 * 48 * 80
+    assert L.psa_blocked_tokens(_lib.grid_of(3, 5, 7, 2), _b3(2, 2, 3)) == 4 * 6 * 9 + 2
+    assert L.psa_blocked_tokens(_lib.grid_of(3, 5, 7), _b3(0, 2, 3)) == -1
+    assert L.psa_blocked_tokens(_lib.grid_of(0, 5, 7), _b3(1, 2, 3)) == -1
+    ws = L.psa_workspace_size_3d(1, 40, _lib.grid_of(21, 45, 80), _b3(3, 8, 16), 128)
+    assert ws >= 16 * (21 * 48 * 80 // 128) and ws % 256 == 0
+    assert L.psa_workspace_size_3d(1, 40, _lib.grid_of(21, 45, 80), _b3(3, 8, 5), 128) == 0   # 120 % 128
+    assert L.psa_workspace_size_3d(1, 40, _lib.grid_of(21, 45, 80), _b3(3, 8, 16), 32) == 0
+
+
+def test_layout_validation_codes():
+    L = _lib.lib()
+    vp = ctypes.c_void_p
+    g = _lib.grid_of(3, 5, 7, 2)
+    assert L.psa_to_blocks(None, vp(256), 1, 128, g, _b3(2, 2, 2), None) == _lib.PSA_ERR_INVALID
+    assert L.psa_from_blocks(vp(256), None, 1, 128, g, _b3(2, 2, 2), None) == _lib.PSA_ERR_INVALID
+    assert L.psa_to_blocks(vp(256), vp(256), 0, 128, g, _b3(2, 2, 2), None) == _lib.PSA_ERR_INVALID
+    assert L.psa_to_blocks(vp(256), vp(256), 1, 96, g, _b3(2, 2, 2), None) == _lib.PSA_ERR_UNSUPPORTED
+    assert L.psa_to_blocks(vp(256), vp(256), 1, 64, g, _b3(2, 0, 2), None) == _lib.PSA_ERR_INVALID
+    assert L.psa_to_blocks(vp(256), vp(256), 70000, 64, g, _b3(2, 2, 2), None) == _lib.PSA_ERR_UNSUPPORTED
+    assert L.psa_build_blockmap_3d(_lib.stripes([(1, 0, 0, 1, 0, 1)]), 1, g, _b3(2, 2, 2), None, None,
+                                   None, None) == _lib.PSA_ERR_INVALID
+
+
+def test_plan_and_run_3d_validation_codes():
+    L = _lib.lib()
+    vp = lambda x: ctypes.c_void_p(x) if x else None
+    g = _lib.grid_of(4, 10, 20, 0)
+    ok = [(1, 0, INF, 1, 0, INF)]
+
+    def plan(pb=(2, 4, 16), tile=128, params=ok, ws=256, wsb=1 << 20, batch=1):
+        return L.psa_attention_plan_3d(batch, len(params), g, _b3(*pb), tile, _lib.stripes(params),
+                                       vp(ws), wsb, None, None)
+
+    assert plan(tile=32) == _lib.PSA_ERR_UNSUPPORTED
+    assert plan(pb=(3, 8, 5)) == _lib.PSA_ERR_UNSUPPORTED          # 120 positions: not whole tiles
+    assert plan(pb=(1, 0, 16)) == _lib.PSA_ERR_INVALID
+    assert plan(params=[(1, 0, 1, 1, 0, 0)]) == _lib.PSA_ERR_INVALID
+    assert plan(ws=0) == _lib.PSA_ERR_WORKSPACE
+    assert plan(wsb=64) == _lib.PSA_ERR_WORKSPACE
+    assert plan(batch=0) == _lib.PSA_ERR_INVALID
+
+    def run(q=256, d=128, tile=128, pb=(2, 4, 16)):
+        return L.psa_attention_run_3d(vp(q), vp(256), vp(256), vp(256), 1, 1, d, g, _b3(*pb), tile,
+                                      0.1, vp(256), 1 << 20, None, None)
+
+    assert run(q=0) == _lib.PSA_ERR_INVALID
+    assert run(d=80) == _lib.PSA_ERR_UNSUPPORTED
+    assert run(tile=96) == _lib.PSA_ERR_UNSUPPORTED
+    assert run(pb=(1, 3, 5)) == _lib.PSA_ERR_UNSUPPORTED

@@ -21,6 +21,19 @@ def test_stored_densities_match_oracle_blockmap(name):
     assert dens.min() >= lo - 0.01 and dens.max() <= hi + 0.01
 
 
+def test_psablock_workload_densities_match_oracle_map():
+    cfg = get_config("wan14b_3d")
+    params = stripe_params("wan14b_3d")
+    assert len(params) == cfg.heads and cfg.coarse_grid == (7, 6, 5)
+    bm = oracle.psablock_map(params, cfg.frames, cfg.height, cfg.width, cfg.n_text, cfg.psablock)
+    dens = bm.reshape(cfg.heads, -1).sum(1) / float(bm.shape[1] ** 2)
+    np.testing.assert_allclose(dens, load_json()["wan14b_3d"]["density"], rtol=0, atol=1e-12)
+    tp, sp = coarse_extent(cfg)
+    assert (tp, sp) == (7, 30)
+    for m in params:
+        assert 1 <= m[0] <= tp and 1 <= m[3] <= sp
+
+
 def test_headline_mean_density_near_quarter():
     assert abs(np.mean(load_json()["wan14b"]["density"]) - 0.25) < 0.03
 
@@ -42,7 +55,7 @@ def test_sweep_runs():
 def test_stored_params_regenerate():
     data = msp.build()
     stored = load_json()
-    for name in ("wan1_3b", "wan14b", "hunyuan"):
+    for name in ("wan1_3b", "wan14b", "hunyuan", "wan14b_3d"):
         assert data[name]["params"] == stored[name]["params"]
     assert data["sweep"]["0.30"]["params"] == stored["sweep"]["0.30"]["params"]
 

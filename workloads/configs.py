@@ -6,6 +6,9 @@
 * ``hunyuan``   -- HunyuanVideo 720p joint attention: 1 x 24 heads, d=128, grid 33x45x80 plus
                    256 text tokens appended (N=119056), block 128.
 * ``sweep``     -- the Wan 2.1 14B shape with eight forced kept-tile densities.
+* ``wan14b_3d`` -- the Wan 2.1 14B layer in the paper's own PSABlock layout: 3x8x16 PSABlocks,
+                   the grid 3D-padded to 21x48x80 (appendix on mask-candidate initialisation),
+                   attention tiles of 128 positions; same Q/K/V as ``wan14b``.
 
 The model shapes follow the paper's experimental setup (Sec. 4, "Models"; the latent grids
 21x45x80 and 33x45x80 appear in the appendix on mask-candidate initialisation).
@@ -27,6 +30,7 @@ class Config:
     rope_split: tuple          # channels per axis (t, h, w) of the 3D rotary embedding
     density_band: tuple        # (lo, hi) of the per-head kept-tile density targets, or None
     seed: int = 0              # seed of the Q/K/V draws
+    psablock: tuple = None     # (bt, bh, bw) for the PSABlock-centric layout; `block` is the tile
 
     @property
     def n_video(self) -> int:
@@ -49,6 +53,19 @@ class Config:
     def scale(self) -> float:
         return self.head_dim ** -0.5
 
+    @property
+    def coarse_grid(self) -> tuple:
+        """(T', H', W') of the PSABlock layout (3D padding: ceil of each axis)."""
+        bt, bh, bw = self.psablock
+        return (-(-self.frames // bt), -(-self.height // bh), -(-self.width // bw))
+
+    @property
+    def n_blocked(self) -> int:
+        """Positions of the PSABlock-centric layout."""
+        tp, hp, wp = self.coarse_grid
+        bt, bh, bw = self.psablock
+        return tp * hp * wp * bt * bh * bw + self.n_text
+
 
 SWEEP_TARGETS = (0.05, 0.10, 0.20, 0.30, 0.50, 0.70, 0.90, 1.00)
 
@@ -58,6 +75,8 @@ CONFIGS = {
     "wan14b": Config("wan14b", 1, 40, 128, 21, 45, 80, 0, 128, (44, 42, 42), (0.10, 0.40)),
     "hunyuan": Config("hunyuan", 1, 24, 128, 33, 45, 80, 256, 128, (44, 42, 42), (0.10, 0.35)),
     "sweep": Config("sweep", 1, 40, 128, 21, 45, 80, 0, 128, (44, 42, 42), None),
+    "wan14b_3d": Config("wan14b_3d", 1, 40, 128, 21, 45, 80, 0, 128, (44, 42, 42), (0.10, 0.40),
+                        psablock=(3, 8, 16)),
 }
 
 

@@ -9,7 +9,7 @@ f_T . C . f_S + (tiles touching a global block), where C[dt, ds] counts ordered 
 non-global blocks at distance (dt, ds); this is exact, and ``tests/test_workloads.py`` checks
 it against the oracle's full block map.
 
-* wan1_3b / wan14b / hunyuan: head h draws a target density rho_h ~ U[lo, hi] with
+* wan1_3b / wan14b / hunyuan / wan14b_3d (densities of PSABlock pairs): head h draws a target density rho_h ~ U[lo, hi] with
   ``default_rng([1, config index])``; among all candidate tuples (paper ranges, widths
   1..extent) within 0.5 % of the closest achievable density, one is drawn at random.
 * sweep: eight runs with every head forced to 5,10,20,30,50,70,90,100 %; head h uses
@@ -36,7 +36,10 @@ CONFIG_INDEX = {name: i for i, name in enumerate(CONFIGS)}
 
 
 def pair_histogram(cfg):
-    t, s, _, g = oracle.block_coordinates(cfg.frames, cfg.height, cfg.width, cfg.n_text, cfg.block)
+    if cfg.psablock is not None:
+        t, s, g = oracle.group_coordinates(cfg.frames, cfg.height, cfg.width, cfg.n_text, cfg.psablock)
+    else:
+        t, s, _, g = oracle.block_coordinates(cfg.frames, cfg.height, cfg.width, cfg.n_text, cfg.block)
     tp, sp = coarse_extent(cfg)
     tv, sv = t[~g], s[~g]
     dt = (tv[None, :] - tv[:, None]).ravel() + (tp - 1)
@@ -103,7 +106,7 @@ def sweep(cfg, seed):
 
 def build():
     data = {}
-    for name in ("wan1_3b", "wan14b", "hunyuan"):
+    for name in ("wan1_3b", "wan14b", "hunyuan", "wan14b_3d"):
         data[name] = targeted(CONFIGS[name], [1, CONFIG_INDEX[name]])
     data["sweep"] = sweep(CONFIGS["sweep"], [1, CONFIG_INDEX["sweep"]])
     return data
@@ -114,7 +117,7 @@ if __name__ == "__main__":
     path = os.path.join(ROOT, "workloads", "stripe_params.json")
     with open(path, "w") as f:
         json.dump(data, f, indent=1)
-    for name in ("wan1_3b", "wan14b", "hunyuan"):
+    for name in ("wan1_3b", "wan14b", "hunyuan", "wan14b_3d"):
         d = data[name]["density"]
         print(name, "mean density %.4f  min %.4f  max %.4f" % (np.mean(d), min(d), max(d)))
     for key, run in data["sweep"].items():

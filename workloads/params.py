@@ -1,7 +1,8 @@
 """Per-head stripe parameters M = (T_w, T_o, T_s, S_w, S_o, S_s) for each workload.
 
 Units: temporal parameters count frames, spatial parameters count block slots within a frame
-(a frame of H*W tokens holds ceil(H*W / block) slots).  The candidate ranges are the paper's
+(a frame of H*W tokens holds ceil(H*W / block) slots); for the PSABlock workload they count
+PSABlocks along time and PSABlocks of the H' x W' plane.  The candidate ranges are the paper's
 (appendix, "Initialization of Mask Candidates"): T_o in {0,+-1,+-2}, T_s in {1,2,3,inf},
 S_o in {0,+-1}, S_s in {1,3,5,6,inf}; widths run from 1 to the extent of the axis.
 An infinite stride is encoded as STRIDE_INF = 2^31 - 1.
@@ -25,7 +26,11 @@ _JSON = os.path.join(os.path.dirname(os.path.abspath(__file__)), "stripe_params.
 
 
 def coarse_extent(cfg):
-    """(T', S'): frames, and block slots per frame."""
+    """(T', S'): frames and block slots per frame; with PSABlocks, PSABlocks along time and
+    PSABlocks of the H' x W' plane."""
+    if cfg.psablock is not None:
+        tp, hp, wp = cfg.coarse_grid
+        return tp, hp * wp
     return cfg.frames, -(-(cfg.height * cfg.width) // cfg.block)
 
 
