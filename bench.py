@@ -46,6 +46,9 @@ WORKLOAD_TEXT = {
                "(N=119056), block 128, seeded per-head stripes (kept-tile density 10-35%)",
     "sweep": "Wan 2.1 14B shape (B=1, 40 heads, d=128, N=75600), every head forced to one kept-tile "
              "density",
+    "wan14b_3d": "Wan 2.1 14B 720p attention layer in the PSABlock-centric layout: B=1, 40 heads, "
+                 "d=128, grid 21x45x80 3D-padded to 21x48x80, 3x8x16 PSABlocks, tiles of 128, "
+                 "seeded per-head stripes in PSABlock units (PSABlock-pair density 10-40%)",
 }
 
 
@@ -280,6 +283,107 @@ def cpu_baseline(cfg, params, seconds):
     }
 
 
+def group_tokens(cfg):
+    """Tokens of every PSABlock (and of the text group) of a 3D workload, host arithmetic."""
+    bt, bh, bw = cfg.psablock
+    tp, hp, wp = cfg.coarse_grid
+    ext = lambda full, b, n: np.minimum(b, full - b * np.arange(n))
+    cnt = (ext(cfg.frames, bt, tp)[:, None, None] * ext(cfg.height, bh, hp)[None, :, None]
+           * ext(cfg.width, bw, wp)[None, None, :]).ravel().astype(np.float64)
+    return np.append(cnt, float(cfg.n_text)) if cfg.n_text else cnt
+
+
+def bench_3d(args, cfg, params, torch, psa):
+    """The PSABlock-centric path: layout conversion, plan + run, conversion back."""
+    name = cfg.name
+    grid = (cfg.frames, cfg.height, cfg.width, cfg.n_text)
+    pb, tile = cfg.psablock, cfg.block
+    from workloads import make_qkv
+    q, k, v = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to("cuda:0")
+               for x in make_qkv(cfg, workers=16))
+    qb, kb, vb = (psa.to_blocks(x, grid, pb) for x in (q, k, v))
+    ob = torch.empty_like(qb)
+    o = torch.empty_like(q)
+    ws = psa.Workspace3d(cfg.batch, cfg.heads, grid, pb, tile, q.device)
+    bm, _, _ = psa.build_blockmap_3d(params, grid, pb, device=q.device)
+    cnt = torch.from_numpy(group_tokens(cfg)).to(q.device)
+    flops = 4.0 * cfg.head_dim * cfg.batch * (bm.double() * cnt[None, :, None] * cnt[None, None, :]).sum().item()
+    density = bm.double().mean().item()
+
+    def step():
+        psa.attention_fwd_3d(qb, kb, vb, grid, pb, params, tile, cfg.scale, out=ob, workspace=ws)
+
+    t_step = time_calls(step, args.steps, args.warmup, torch)
+    _, kept = psa.plan_3d(params, grid, pb, tile, batch=cfg.batch, workspace=ws, return_kept_per_tile=True)
+    processed = 4.0 * cfg.head_dim * tile * tile * cfg.batch * kept.double().sum().item()
+
+    def kernel_only():
+        psa.run_3d(qb, kb, vb, grid, pb, tile, ws, cfg.scale, out=ob)
+
+    t_kernel = time_calls(kernel_only, args.steps, 1, torch)
+
+    def to_layout():
+        for x, xb in ((q, qb), (k, kb), (v, vb)):
+            psa.to_blocks(x, grid, pb, out=xb)
+
+    def from_layout():
+        psa.from_blocks(ob, grid, pb, out=o)
+
+    t_to = time_calls(to_layout, args.steps, 1, torch)
+    t_from = time_calls(from_layout, args.steps, 1, torch)
+    elem = cfg.batch * cfg.heads * cfg.head_dim * 2.0
+    to_bytes = 3 * (cfg.n_tokens + cfg.n_blocked) * elem
+    from_bytes = (cfg.n_tokens + cfg.n_blocked) * elem
+    ms = t_step["mean"]
+    tflops = flops / (ms * 1e-3) / 1e12
+    k_tflops = flops / (t_kernel["mean"] * 1e-3) / 1e12
+    result = {
+        "metric": "sparse-attn fwd computed TFLOP/s & MFU; speedup vs own dense at Wan-14B shape",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[name], "psablock_pair_density": round(density, 5),
+                   "computed_tflop": round(flops / 1e12, 4), "processed_tflop": round(processed / 1e12, 4),
+                   "blocked_tokens": cfg.n_blocked, "tokens": cfg.n_tokens},
+        "mfu": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "step_ms": {key: round(val, 4) for key, val in t_step.items()},
+        "kernel_ms": {key: round(val, 4) for key, val in t_kernel.items()},
+        "padding_overhead": round(processed / flops - 1.0, 4),
+        "padded_token_ratio": round(cfg.n_blocked / cfg.n_tokens - 1.0, 4),
+        "layout": {"to_blocks_qkv_ms": round(t_to["mean"], 4), "from_blocks_o_ms": round(t_from["mean"], 4),
+                   "to_blocks_gbps": round(to_bytes / (t_to["mean"] * 1e-3) / 1e9, 1),
+                   "from_blocks_gbps": round(from_bytes / (t_from["mean"] * 1e-3) / 1e9, 1),
+                   "hbm_peak_gbps": 8000.0},
+    }
+    log("3d sparse: %.3f ms/step, kernel %.3f ms, %.1f TFLOP/s computed (%.1f processed), density %.4f, "
+        "padding overhead %.3f" % (ms, t_kernel["mean"], tflops, processed / (ms * 1e-3) / 1e12, density,
+                                   processed / flops - 1))
+    log("layout: to_blocks(q,k,v) %.3f ms (%.0f GB/s), from_blocks(o) %.3f ms (%.0f GB/s)"
+        % (t_to["mean"], to_bytes / (t_to["mean"] * 1e-3) / 1e9, t_from["mean"],
+           from_bytes / (t_from["mean"] * 1e-3) / 1e9))
+    if not args.no_dense:
+        def dense():
+            psa.dense_fwd(q, k, v, 128, cfg.scale, out=o)
+        dms = time_calls(dense, args.dense_steps or max(3, args.steps // 2), 1, torch)["mean"]
+        result.update({"dense_ms": round(dms, 4), "speedup_vs_dense": round(dms / ms, 3),
+                       "speedup_vs_dense_with_layout": round(dms / (ms + t_to["mean"] + t_from["mean"]), 3)})
+        log("dense (original order, unpadded): %.3f ms, speedup %.3f (%.3f with the layout conversions)"
+            % (dms, dms / ms, dms / (ms + t_to["mean"] + t_from["mean"])))
+    result["roofline"] = {"kernel": "psa_sparse_kernel<128, 128, true>", "bound": "mfma",
+                          "achieved": round(k_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                          "frac": round(k_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.kernel_stats:
@@ -304,6 +408,8 @@ def main():
     name = args.workload
     cfg = get_config(name)
     params = stripe_params(name, args.target if name == "sweep" else None)
+    if cfg.psablock is not None:
+        return bench_3d(args, cfg, params, torch, psa)
     grid = (cfg.frames, cfg.height, cfg.width, cfg.n_text)
     log("workload %s: generating inputs" % name)
     t0 = time.perf_counter()

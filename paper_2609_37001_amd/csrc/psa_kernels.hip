@@ -201,17 +201,28 @@ __global__ __launch_bounds__(256) void psa_layout_kernel(const uint4* __restrict
     const int32_t vol = g.pbt * area;
     const int32_t tq = pb / plane, r = pb - tq * plane, hq = r / g.wp, wq = r - hq * g.wp;
     const int32_t t0 = tq * g.pbt, h0 = hq * g.pbh, w0 = wq * g.pbw;
-    for (int32_t e = threadIdx.x; e < vol * CPR; e += 256) {
-      const int32_t x = e / CPR, c = e % CPR;
-      const int32_t it = x / area, r2 = x - it * area, ih = r2 / g.pbw, iw = r2 - ih * g.pbw;
-      const int32_t t = t0 + it, h = h0 + ih, w = w0 + iw;
-      const bool valid = t < g.frames && h < g.height && w < g.width;
-      const size_t orow = ((size_t)t * g.height + h) * g.width + w;
-      const size_t brow = (size_t)pb * vol + x;
-      if (TO)
-        d[brow * CPR + c] = valid ? s[orow * CPR + c] : make_uint4(0u, 0u, 0u, 0u);
-      else if (valid)
-        d[orow * CPR + c] = s[brow * CPR + c];
+    // Four 16-byte chunks per thread and round: every load is issued before the first store.
+    for (int32_t e0 = threadIdx.x; e0 < vol * CPR; e0 += 4 * 256) {
+      size_t from[4], to[4];
+      bool live[4];
+      uint4 val[4];
+#pragma unroll
+      for (int u = 0; u < 4; u++) {
+        const int32_t e = e0 + u * 256;
+        const int32_t x = e / CPR, c = e % CPR;
+        const int32_t it = x / area, r2 = x - it * area, ih = r2 / g.pbw, iw = r2 - ih * g.pbw;
+        const int32_t t = t0 + it, h = h0 + ih, w = w0 + iw;
+        const bool valid = e < vol * CPR && t < g.frames && h < g.height && w < g.width;
+        const size_t orow = ((size_t)t * g.height + h) * g.width + w;
+        const size_t brow = (size_t)pb * vol + x;
+        from[u] = (TO ? orow : brow) * CPR + c;
+        to[u] = (TO ? brow : orow) * CPR + c;
+        live[u] = TO ? e < vol * CPR : valid;
+        val[u] = valid ? s[from[u]] : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; u++)
+        if (live[u]) d[to[u]] = val[u];
     }
   } else {
     const int32_t r0 = ((int32_t)blockIdx.x - n_p) * 64;
