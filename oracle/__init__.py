@@ -13,6 +13,8 @@ imports nothing from it.  Everything here is plain numpy, computed in float64:
 * ``psablock``  -- 3D PSABlocks with 3D padding (Sec. 3.2): the PSABlock grid, the group of
                    every original token, Algorithm 1 on the PSABlock grid, and the
                    PSABlock-centric (T', H', W', bt, bh, bw) layout.
+* ``search``    -- PSA-Search (Algorithm 3) and its dual interface: per-head relative L2 loss
+                   of a candidate against full attention, and the selection rules.
 
 Every function is pinned by tests against values fixed by the paper and by mathematics
 (hand-worked maps, closed-form counts, symmetry and periodicity invariants, library softmax
@@ -23,3 +25,4 @@ from .stripe import (STRIDE_INF, axis_condition, is_attending, block_coordinates
 from .attention import masked_attention  # noqa: F401
 from .psablock import (psablock_grid, token_groups, group_coordinates,  # noqa: F401
                        psablock_map, to_blocks, from_blocks)
+from . import search  # noqa: F401

@@ -102,3 +102,16 @@ def test_rope_rotates_pairs():
     n_raw = np.hypot(raw[:24, 0::2], raw[:24, 1::2])
     np.testing.assert_allclose(n_rot, n_raw, rtol=2e-2, atol=1e-2)
     assert (q[0] == raw[0]).all()                         # position (0,0,0): angle 0
+
+
+def test_search_candidates_in_paper_space():
+    from workloads.candidates import candidates
+    cfg = get_config("wan14b")
+    tp, sp = coarse_extent(cfg)
+    cands = candidates("wan14b", 100)
+    assert len(cands) == cfg.heads and all(len(c) == 100 and len(set(c)) == 100 for c in cands)
+    for head in cands:
+        for m in head:
+            assert 1 <= m[0] <= tp and m[1] in (0, 1, -1, 2, -2) and m[2] in (1, 2, 3, STRIDE_INF)
+            assert 1 <= m[3] <= sp and m[4] in (0, 1, -1) and m[5] in (1, 3, 5, 6, STRIDE_INF)
+    assert cands[0] != cands[1] and candidates("wan14b", 100) == cands
