@@ -71,6 +71,8 @@ def parse():
                    help="run one plain device copy of this many MiB first (counter calibration)")
     p.add_argument("--counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) and exit")
+    p.add_argument("--search", type=int, default=0, metavar="K",
+                   help="time PSA-Search scoring of K candidates per head (all heads per call)")
     p.add_argument("--kernel-stats", metavar="TRACE_DIR",
                    help="print the kernel table of a rocprofv3 --kernel-trace --stats csv run and exit")
     p.add_argument("--utilisation", nargs=3, metavar=("SQ_DIR", "TCC_DIR", "TRACE_DIR"),
@@ -384,6 +386,61 @@ def bench_3d(args, cfg, params, torch, psa):
     return 0
 
 
+def bench_search(args, cfg, torch, psa):
+    """PSA-Search scoring: per candidate, one sparse call for all heads, the L2 reduction
+    against the dense output, and the kept counts for the sparsity."""
+    from paper_2609_37001_amd import search
+    from workloads import make_qkv
+    from workloads.candidates import candidates
+    grid = (cfg.frames, cfg.height, cfg.width, cfg.n_text)
+    q, k, v = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to("cuda:0")
+               for x in make_qkv(cfg, workers=16))
+    cands = [c[:args.search] for c in candidates(cfg.name, max(args.search, 1))]
+    search.score(q, k, v, grid, cfg.block, [c[:1] for c in cands], cfg.scale)        # warm-up
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    res = search.score(q, k, v, grid, cfg.block, cands, cfg.scale)
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end)
+    full = psa.dense_fwd(q, k, v, cfg.block, cfg.scale)
+    o = torch.empty_like(q)
+    t_l2 = time_calls(lambda: psa.l2_distance(o, full), args.steps, 2, torch)
+    l2_bytes = 2.0 * q.numel() * 2
+    per_cand = ms / args.search
+    picks = search.select(res, 0.02)
+    result = {
+        "metric": "PSA-Search scoring: candidate evaluations per second (all heads per evaluation)",
+        "value": round(1e3 / per_cand, 3),
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.search,
+        "warmup": 1,
+        "ms_per_step": round(per_cand, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[cfg.name] + "; %d candidates per head from the paper's "
+                               "candidate space" % args.search,
+                   "includes": "dense reference once, per candidate: plan + sparse kernel + L2 + kept counts"},
+        "wall_s": round(wall, 3),
+        "extrapolated_s_per_100_candidates": round(per_cand * 100 / 1e3, 2),
+        "mean_candidate_sparsity": round(float(res.sparsity.mean()), 4),
+        "mean_selected_sparsity_alpha_0.02": round(float(np.mean([res.sparsity[h][i] for h, i in enumerate(picks)])), 4),
+        "l2_kernel": {"ms": round(t_l2["mean"], 4), "gbps": round(l2_bytes / (t_l2["mean"] * 1e-3) / 1e9, 1),
+                      "hbm_peak_gbps": 8000.0},
+    }
+    log("search: %d candidates x %d heads in %.1f ms (%.2f ms per candidate), L2 kernel %.3f ms (%.0f GB/s)"
+        % (args.search, cfg.heads, ms, per_cand, t_l2["mean"], l2_bytes / (t_l2["mean"] * 1e-3) / 1e9))
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.kernel_stats:
@@ -410,6 +467,8 @@ def main():
     params = stripe_params(name, args.target if name == "sweep" else None)
     if cfg.psablock is not None:
         return bench_3d(args, cfg, params, torch, psa)
+    if args.search:
+        return bench_search(args, cfg, torch, psa)
     grid = (cfg.frames, cfg.height, cfg.width, cfg.n_text)
     log("workload %s: generating inputs" % name)
     t0 = time.perf_counter()

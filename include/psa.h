@@ -220,6 +220,28 @@ psa_status_t psa_attention_run_3d(const void* q, const void* k, const void* v, v
                                   float softmax_scale, void* workspace, size_t workspace_bytes,
                                   float* lse, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------------------------
+ * PSA-Search scoring (Algorithm 3 in the appendix "Process of PSA-Search"; Sec. 3.3): the L2
+ * loss between a head's sparse attention output under a candidate mask and its full attention
+ * output.  A search evaluates each candidate with psa_attention_fwd (one candidate per head per
+ * call) against psa_dense_fwd, and reduces both outputs here.
+ * --------------------------------------------------------------------------------------------- */
+
+/* Bytes of device workspace of psa_l2_distance (0 if batch_heads < 1). */
+size_t psa_l2_workspace_size(int32_t batch_heads);
+
+/* Per (batch, head) row r: sq_err[r] = sum over tokens and channels of (o - ref)^2 and
+ * sq_ref[r] = sum of ref^2 (relative L2 loss = sqrt(sq_err / sq_ref)).  Products and sums in
+ * fp32 within 64 chunks per row, combined in fp64 in a fixed order: the result is
+ * deterministic.
+ *   o, ref          device bf16 [batch_heads][n_tokens][head_dim], 16-byte aligned
+ *   sq_err, sq_ref  device double [batch_heads] (sq_ref may be NULL)
+ *   workspace       device, psa_l2_workspace_size(batch_heads) bytes, 8-byte aligned
+ * head_dim a multiple of 8, batch_heads <= 65535. */
+psa_status_t psa_l2_distance(const void* o, const void* ref, int32_t batch_heads, int32_t n_tokens,
+                             int32_t head_dim, double* sq_err, double* sq_ref, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* psa_status_string(psa_status_t status);
 

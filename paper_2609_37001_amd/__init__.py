@@ -27,7 +27,7 @@ from ._lib import STRIDE_INF, PsaError  # noqa: F401
 __all__ = ["STRIDE_INF", "PsaError", "num_blocks", "workspace_size", "build_blockmap",
            "attention_fwd", "plan", "run", "dense_fwd", "Workspace", "library_path",
            "blocked_tokens", "to_blocks", "from_blocks", "build_blockmap_3d", "plan_3d", "run_3d",
-           "attention_fwd_3d"]
+           "attention_fwd_3d", "l2_distance"]
 
 
 def library_path():
@@ -343,3 +343,27 @@ def attention_fwd_3d(q, k, v, grid, pb, params, tile=128, scale=None, out=None, 
     b = q.shape[0]
     ws = plan_3d(params, grid, pb, tile, batch=b, device=q.device, workspace=workspace, stream=stream)
     return run_3d(q, k, v, grid, pb, tile, ws, scale, out, return_lse, stream)
+
+
+# ---------------------------------------------------------------------------------------------
+# PSA-Search scoring (include/psa.h, third part); the search itself is in .search.
+# ---------------------------------------------------------------------------------------------
+
+def l2_distance(o, ref, sq_err=None, sq_ref=None, workspace=None, stream=None):
+    """Per (batch, head) sums of (o - ref)^2 and ref^2 (float64 [batch, heads] each)."""
+    torch = _torch()
+    _check_qkv(o, ref)
+    b, h, n, d = o.shape
+    err = torch.empty((b, h), dtype=torch.float64, device=o.device) if sq_err is None else sq_err
+    rref = torch.empty((b, h), dtype=torch.float64, device=o.device) if sq_ref is None else sq_ref
+    for t in (err, rref):
+        if t.dtype != torch.float64 or t.numel() != b * h or not t.is_contiguous():
+            raise ValueError("sq_err and sq_ref must be contiguous float64 tensors of %d elements" % (b * h))
+    nbytes = int(_lib.lib().psa_l2_workspace_size(b * h))
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=o.device) if workspace is None else workspace
+    if ws.numel() < nbytes:
+        raise ValueError("l2 workspace needs %d bytes" % nbytes)
+    with torch.cuda.device(o.device):
+        _lib.check(_lib.lib().psa_l2_distance(_ptr(o), _ptr(ref), b * h, n, d, _ptr(err), _ptr(rref),
+                                              _ptr(ws), ws.numel(), _stream(stream, o.device)))
+    return err, rref

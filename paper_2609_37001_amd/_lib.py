@@ -24,7 +24,8 @@ PSA_ERR_HIP = 4
 EXPORTS = ("psa_num_blocks", "psa_workspace_size", "psa_build_blockmap", "psa_attention_plan",
            "psa_attention_run", "psa_attention_fwd", "psa_dense_fwd", "psa_blocked_tokens",
            "psa_to_blocks", "psa_from_blocks", "psa_build_blockmap_3d", "psa_workspace_size_3d",
-           "psa_attention_plan_3d", "psa_attention_run_3d", "psa_status_string", "psa_last_error")
+           "psa_attention_plan_3d", "psa_attention_run_3d", "psa_l2_workspace_size", "psa_l2_distance",
+           "psa_status_string", "psa_last_error")
 
 
 class Stripe(ctypes.Structure):
@@ -101,6 +102,10 @@ def lib():
         L.psa_attention_run_3d.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, Block3d, i32,
                                            ctypes.c_float, vp, sz, vp, vp]
         L.psa_attention_run_3d.restype = ctypes.c_int
+        L.psa_l2_workspace_size.argtypes = [i32]
+        L.psa_l2_workspace_size.restype = sz
+        L.psa_l2_distance.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, sz, vp]
+        L.psa_l2_distance.restype = ctypes.c_int
         L.psa_status_string.argtypes = [ctypes.c_int]
         L.psa_status_string.restype = ctypes.c_char_p
         L.psa_last_error.argtypes = []

@@ -398,6 +398,31 @@ psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o,
   return PSA_OK;
 }
 
+size_t psa_l2_workspace_size(int32_t batch_heads) {
+  return batch_heads < 1 ? 0 : (size_t)batch_heads * psa::kL2Chunks * 2 * sizeof(double);
+}
+
+psa_status_t psa_l2_distance(const void* o, const void* ref, int32_t batch_heads, int32_t n_tokens,
+                             int32_t head_dim, double* sq_err, double* sq_ref, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  if (!o || !ref || !sq_err) return fail(PSA_ERR_INVALID, "o, ref and sq_err must be non-NULL");
+  if (batch_heads < 1 || n_tokens < 1)
+    return fail(PSA_ERR_INVALID, "batch_heads and n_tokens must be >= 1 (got %d, %d)", batch_heads,
+                n_tokens);
+  if (batch_heads > 65535)
+    return fail(PSA_ERR_UNSUPPORTED, "batch_heads must be <= 65535 (got %d)", batch_heads);
+  if (head_dim < 8 || head_dim % 8 != 0)
+    return fail(PSA_ERR_UNSUPPORTED, "head_dim must be a positive multiple of 8 (got %d)", head_dim);
+  if (((uintptr_t)o & 15) != 0 || ((uintptr_t)ref & 15) != 0)
+    return fail(PSA_ERR_INVALID, "o and ref must be 16-byte aligned");
+  if (!workspace || workspace_bytes < psa_l2_workspace_size(batch_heads))
+    return fail(PSA_ERR_WORKSPACE, "workspace of %zu bytes; %zu bytes required", workspace_bytes,
+                psa_l2_workspace_size(batch_heads));
+  hipError_t e = psa::launch_l2(o, ref, batch_heads, (int64_t)n_tokens * head_dim, (double*)workspace,
+                                sq_err, sq_ref, stream);
+  return e == hipSuccess ? PSA_OK : hip_fail(e, "psa_l2_distance launch");
+}
+
 const char* psa_status_string(psa_status_t status) {
   switch (status) {
     case PSA_OK: return "PSA_OK";

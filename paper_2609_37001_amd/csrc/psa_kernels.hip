@@ -189,6 +189,79 @@ hipError_t launch_group_blockmap(const ParamChunk& pc, int32_t head0, const Geom
 // read in order, the original side in runs of bw rows.
 // ---------------------------------------------------------------------------------------------
 
+// ---------------------------------------------------------------------------------------------
+// L2 distance per (batch, head) (the loss of PSA-Search).
+// ---------------------------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Fixed-order sum over a 256-thread workgroup (butterfly in each wave, then the four waves).
+__device__ __forceinline__ double block_sum(double x, double* red) {
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  const double t = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return t;
+}
+
+__global__ __launch_bounds__(256) void psa_l2_partial_kernel(const uint4* __restrict__ o,
+                                                             const uint4* __restrict__ ref,
+                                                             int64_t vec_per_bh,
+                                                             double* __restrict__ partial) {
+  __shared__ double red[4];
+  const int64_t per = (vec_per_bh + kL2Chunks - 1) / kL2Chunks;
+  const int64_t lo = (int64_t)blockIdx.x * per, hi = min(lo + per, vec_per_bh);
+  const uint4* a = o + (int64_t)blockIdx.y * vec_per_bh;
+  const uint4* b = ref + (int64_t)blockIdx.y * vec_per_bh;
+  float se = 0.0f, sr = 0.0f;
+  for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
+    const uint4 x = a[i], y = b[i];
+    const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const float r0 = bf16_lo(ys[j]), r1 = bf16_hi(ys[j]);
+      const float d0 = bf16_lo(xs[j]) - r0, d1 = bf16_hi(xs[j]) - r1;
+      se = __builtin_fmaf(d0, d0, __builtin_fmaf(d1, d1, se));
+      sr = __builtin_fmaf(r0, r0, __builtin_fmaf(r1, r1, sr));
+    }
+  }
+  const double te = block_sum(se, red), tr = block_sum(sr, red);
+  if (threadIdx.x == 0) {
+    double* dst = partial + ((int64_t)blockIdx.y * kL2Chunks + blockIdx.x) * 2;
+    dst[0] = te;
+    dst[1] = tr;
+  }
+}
+
+__global__ __launch_bounds__(64) void psa_l2_final_kernel(const double* __restrict__ partial,
+                                                          double* __restrict__ sq_err,
+                                                          double* __restrict__ sq_ref) {
+  const double* p = partial + (int64_t)blockIdx.x * kL2Chunks * 2;
+  double e = p[2 * threadIdx.x], r = p[2 * threadIdx.x + 1];
+  for (int off = 32; off > 0; off >>= 1) {
+    e += __shfl_xor(e, off);
+    r += __shfl_xor(r, off);
+  }
+  if (threadIdx.x == 0) {
+    sq_err[blockIdx.x] = e;
+    if (sq_ref) sq_ref[blockIdx.x] = r;
+  }
+}
+
+hipError_t launch_l2(const void* o, const void* ref, int32_t n_bh, int64_t elems_per_bh,
+                     double* partial, double* sq_err, double* sq_ref, hipStream_t stream) {
+  static_assert(kL2Chunks == 64, "the final pass sums one partial per lane of a wave");
+  hipLaunchKernelGGL(psa_l2_partial_kernel, dim3(kL2Chunks, (unsigned)n_bh), dim3(256), 0, stream,
+                     (const uint4*)o, (const uint4*)ref, elems_per_bh / 8, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(psa_l2_final_kernel, dim3((unsigned)n_bh), dim3(64), 0, stream, partial, sq_err,
+                     sq_ref);
+  return hipGetLastError();
+}
+
 template <bool TO, int CPR>
 __global__ __launch_bounds__(256) void psa_layout_kernel(const uint4* __restrict__ src,
                                                          uint4* __restrict__ dst, Geometry g) {

@@ -90,6 +90,14 @@ hipError_t launch_group_blockmap(const ParamChunk& pc, int32_t head0, const Geom
                                  uint8_t* blockmap, int32_t* kept_per_row, int64_t* kept_per_head,
                                  hipStream_t stream);
 
+// Chunks per (batch, head) of the L2 distance's first pass.
+constexpr int kL2Chunks = 64;
+
+// Per (batch, head) sums of (o - ref)^2 and ref^2 over [tokens][d] bf16 rows: fp32 partial sums
+// per chunk, combined in fp64 in a fixed order (partial: kL2Chunks * 2 doubles per row).
+hipError_t launch_l2(const void* o, const void* ref, int32_t n_bh, int64_t elems_per_bh,
+                     double* partial, double* sq_err, double* sq_ref, hipStream_t stream);
+
 // PSABlock-centric layout of [bh][tokens][d] tensors (to: original -> blocked, else back).
 hipError_t launch_layout(const void* src, void* dst, int32_t n_bh, int32_t head_dim,
                          const Geometry& g, bool to_blocks, hipStream_t stream);
