@@ -18,7 +18,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from . import _lib, attention_fwd, build_blockmap, dense_fwd, l2_distance, Workspace
+from . import _lib, attention_fwd, dense_fwd, l2_distance, Workspace
 
 
 @dataclass
@@ -45,11 +45,11 @@ def score(q, k, v, grid, block, candidates, scale=None, stream=None):
     kept = torch.empty((n_cand, h), dtype=torch.int64, device=q.device)
     for c in range(n_cand):
         params = [candidates[hh][c] for hh in range(h)]
-        attention_fwd(q, k, v, grid, block, params, scale, out=o, workspace=ws, stream=stream)
+        # the plan's per-row kept counts give the sparsity without another pass over the map
+        _, per_row = attention_fwd(q, k, v, grid, block, params, scale, out=o, workspace=ws,
+                                   return_kept_per_row=True, stream=stream)
         l2_distance(o, full, sq_err=sq_err[c], sq_ref=sq_ref, workspace=l2_ws, stream=stream)
-        _, _, ph = build_blockmap(params, grid, block, device=q.device, blockmap=False, per_row=False,
-                                  stream=stream)
-        kept[c] = ph
+        kept[c] = per_row.sum(dim=1)
     err = sq_err.sum(dim=1).cpu().numpy()                 # [C, heads]: over batch elements
     ref = sq_ref.sum(dim=0).cpu().numpy()                 # [heads]
     nb = -(-n // block)
