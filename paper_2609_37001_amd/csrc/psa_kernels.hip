@@ -763,6 +763,10 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
   }
 
   // s holds S - base with base = -negm (the running max, or 0 before the first kept key).
+  // The softmax and its P V form the longest dependent chain of a block; while a wave runs it,
+  // it issues ahead of the other wave on its SIMD, whose Q K^T MFMAs fill the gaps (measured:
+  // 3 % faster sparse, 2-4 % dense).
+  __builtin_amdgcn_s_setprio(1);
   float mx = -__builtin_inff();
 #pragma unroll
   for (int kt = 0; kt < H::KT; kt++)
@@ -813,6 +817,7 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
       st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p, st.o[dt], 0, 0, 0);
     }
   }
+  __builtin_amdgcn_s_setprio(0);
 }
 
 // One key/value block with a single K and a single V buffer per workgroup:
