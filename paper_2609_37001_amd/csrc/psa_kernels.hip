@@ -609,17 +609,23 @@ __device__ __forceinline__ float pair_sum(float x) {
 }
 
 
-// Direct global->LDS loads of one K or V block.  DMA slot j (1 KB) of the block is loaded by
-// wave j / LPW; its lane l writes LDS bytes [1024 j + 16 l, +16): row (64 j + l) / CPR, physical
-// chunk (64 j + l) % CPR, which holds logical chunk (physical ^ swz(row)).  The loads are issued
-// from inline assembly (SGPR base + 32-bit lane offset, M0 = LDS destination); the compiler does
-// not track them, so every consumer first waits with wait_dma<N>() and a barrier.
+// Direct global->LDS loads of one half (BLK/2 rows) of a K or V block.  DMA slot j (1 KB) of
+// the block covers LDS bytes [1024 j, +1024); lane l writes bytes [1024 j + 16 l, +16): row
+// (64 j + l) / CPR, physical chunk (64 j + l) % CPR, which holds logical chunk (physical ^
+// swz(row)).  The first half of the slots holds rows 0 .. BLK/2-1.  Every wave loads HW = LPW/2
+// slots of each half: slot h*S2 + wave*HW + i for half h, so that each wave issues the same
+// number of loads per half.  The loads are issued from inline assembly (SGPR base + 32-bit lane
+// offset, M0 = LDS destination); the compiler does not track them, so every consumer first
+// waits with wait_dma<N>() and a barrier.
 template <int D, int BLK>
 struct DmaPlan {
   using T = Tile<D, BLK>;
-  uint32_t off[T::LPW];  // byte offset in the block of the 16 bytes this lane loads in slot i
-  uint32_t lds_k;        // LDS byte address of this wave's first slot in the K buffer
-  uint32_t lds_v;        // same in the V buffer
+  static constexpr int HW = T::LPW / 2;                 // slots per wave per half
+  static constexpr int S2 = T::LPW * T::kWaves / 2;     // slots per half
+  static_assert(T::LPW % 2 == 0, "each wave loads whole slots of both halves");
+  uint32_t off[T::LPW];  // byte offset in the block of the 16 bytes this lane loads: [half][i]
+  uint32_t lds_k[2];     // LDS byte address of this wave's first slot of each K half
+  uint32_t lds_v[2];     // same in the V buffer
   int wave, lane;
 
   __device__ __forceinline__ void init(uint32_t k_base, uint32_t v_base, int wave_, int lane_) {
@@ -627,13 +633,17 @@ struct DmaPlan {
     lane = lane_;
 #pragma unroll
     for (int i = 0; i < T::LPW; i++) off[i] = offset(i, BLK);
-    lds_k = k_base + (uint32_t)(wave * T::LPW) * 1024u;
-    lds_v = v_base + (uint32_t)(wave * T::LPW) * 1024u;
+#pragma unroll
+    for (int h = 0; h < 2; h++) {
+      lds_k[h] = k_base + (uint32_t)(h * S2 + wave * HW) * 1024u;
+      lds_v[h] = v_base + (uint32_t)(h * S2 + wave * HW) * 1024u;
+    }
   }
 
-  // Offset of slot i with rows at or past `rows` clamped to row rows - 1.
-  __device__ __forceinline__ uint32_t offset(int i, int rows) const {
-    const int p = (wave * T::LPW + i) * 64 + lane;
+  // Offset of entry idx = half * HW + i, with rows at or past `rows` clamped to row rows - 1.
+  __device__ __forceinline__ uint32_t offset(int idx, int rows) const {
+    const int slot = (idx / HW) * S2 + wave * HW + idx % HW;
+    const int p = slot * 64 + lane;
     const int row = p / T::CPR;
     const int chunk = (p % T::CPR) ^ swz<T::CPR>(row);
     return (uint32_t)(min(row, rows - 1) * T::RB + chunk * 16);
@@ -658,23 +668,23 @@ __device__ __forceinline__ void wait_dma() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// Load rows of block kb of one tensor (K or V) into its LDS buffer.  Rows past the sequence end
-// are clamped to the last row: their scores are masked to -inf, so they are never weighted.
+// Load half h (rows h*BLK/2 ..) of block kb of one tensor (K or V) into its LDS buffer: this
+// wave's HW slots of that half.  Rows past the sequence end are clamped to the last row: their
+// scores are masked to -inf, so they are never weighted.
 template <int D, int BLK>
-__device__ __forceinline__ void issue_block(const DmaPlan<D, BLK>& plan, const __bf16* xh,
-                                            uint32_t lds, int kb, int n) {
-  using T = Tile<D, BLK>;
+__device__ __forceinline__ void issue_half(const DmaPlan<D, BLK>& plan, const __bf16* xh,
+                                           const uint32_t (&lds)[2], int h, int kb, int n) {
+  using P = DmaPlan<D, BLK>;
   kb = __builtin_amdgcn_readfirstlane(kb);
   const int rows = n - kb * BLK;
   const void* base = (const void*)(xh + (size_t)kb * BLK * D);
+  const uint32_t l0 = __builtin_amdgcn_readfirstlane(lds[h]);
   if (rows >= BLK) {
 #pragma unroll
-    for (int i = 0; i < T::LPW; i++)
-      dma16(__builtin_amdgcn_readfirstlane(lds + i * 1024u), plan.off[i], base);
+    for (int i = 0; i < P::HW; i++) dma16(l0 + i * 1024u, plan.off[h * P::HW + i], base);
   } else {
 #pragma unroll
-    for (int i = 0; i < T::LPW; i++)
-      dma16(__builtin_amdgcn_readfirstlane(lds + i * 1024u), plan.offset(i, rows), base);
+    for (int i = 0; i < P::HW; i++) dma16(l0 + i * 1024u, plan.offset(h * P::HW + i, rows), base);
   }
 }
 
@@ -820,11 +830,14 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
   __builtin_amdgcn_s_setprio(0);
 }
 
-// One key/value block with a single K and a single V buffer per workgroup:
-//   QK(lo) | wait V(i), barrier | softmax+PV(lo), QK(hi) | barrier, load K(i+1) |
-//   softmax+PV(hi) | wait K(i+1), barrier, load V(i+1)
-// K(i+1) streams in during the second half of block i, V(i+1) during QK(lo) of block i+1; the
-// other workgroup on the CU covers the rest of the load latency.
+// One key/value block with a single K and a single V buffer per workgroup, loaded by halves
+// (BLK/2 keys) and three barriers per block:
+//   QK(lo)          | wait V_lo(i), K_hi(i); barrier b1; load K_lo(i+1)
+//   softmax+PV(lo), QK(hi) | wait V_hi(i);   barrier b2; load V_lo(i+1), K_hi(i+1)
+//   softmax+PV(hi)  | wait K_lo(i+1);        barrier b3; load V_hi(i+1)
+// A half is loaded at the first barrier after its last reader and awaited at the last barrier
+// before its first reader, so every load is in flight for two or three phases.  Each wait leaves
+// the loads issued after the awaited ones in flight (HW per half); the last block issues none.
 template <int D, int BLK, bool PAD>
 __device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<D, BLK>& plan,
                                            const __bf16* kh, const __bf16* vh, int kb, int kb_next,
@@ -841,18 +854,30 @@ __device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<
     tail = (kb + 1) * BLK > n;
   }
   using H = Half<D, BLK>;
+  constexpr int HW = DmaPlan<D, BLK>::HW;
+  const bool more = kb_next >= 0;
   f32x16 s[H::KT];
   qk_half<D, BLK>(st, s, sk, 0, lane);
-  wait_dma<0>();
+  wait_dma<HW>();                                       // V_lo(i), K_hi(i); V_hi(i) may fly
   __syncthreads();
+  if (more) issue_half<D, BLK>(plan, kh, plan.lds_k, 0, kb_next, n);
   softmax_pv_half<D, BLK, PAD>(st, s, sv, kb, 0, n, tail, lo, hi, lane);
   qk_half<D, BLK>(st, s, sk, H::HK, lane);
+  if (more)                                             // V_hi(i); K_lo(i+1) may fly
+    wait_dma<HW>();
+  else
+    wait_dma<0>();
   __syncthreads();
-  if (kb_next >= 0) issue_block<D, BLK>(plan, kh, plan.lds_k, kb_next, n);
+  if (more) {
+    issue_half<D, BLK>(plan, vh, plan.lds_v, 0, kb_next, n);
+    issue_half<D, BLK>(plan, kh, plan.lds_k, 1, kb_next, n);
+  }
   softmax_pv_half<D, BLK, PAD>(st, s, sv, kb, H::HK, n, tail, lo, hi, lane);
-  wait_dma<0>();
-  __syncthreads();
-  if (kb_next >= 0) issue_block<D, BLK>(plan, vh, plan.lds_v, kb_next, n);
+  if (more) {
+    wait_dma<2 * HW>();                                 // K_lo(i+1); V_lo, K_hi(i+1) may fly
+    __syncthreads();
+    issue_half<D, BLK>(plan, vh, plan.lds_v, 1, kb_next, n);
+  }
 }
 
 // One work item: query block qb of one (batch, head).  `list` holds the kept key blocks in
@@ -896,9 +921,12 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
   // ascending list.
   auto kv = [&](int i) { return SPARSE ? (int)list[i] : i; };
   if (nkv > 0) {
-    issue_block<D, BLK>(plan, kh, plan.lds_k, kv(0), n);
-    issue_block<D, BLK>(plan, vh, plan.lds_v, kv(0), n);
-    wait_dma<T::LPW>();
+    constexpr int HW = DmaPlan<D, BLK>::HW;
+    issue_half<D, BLK>(plan, kh, plan.lds_k, 0, kv(0), n);
+    issue_half<D, BLK>(plan, vh, plan.lds_v, 0, kv(0), n);
+    issue_half<D, BLK>(plan, kh, plan.lds_k, 1, kv(0), n);
+    issue_half<D, BLK>(plan, vh, plan.lds_v, 1, kv(0), n);
+    wait_dma<3 * HW>();                                 // K_lo(0)
     __syncthreads();
   }
   for (int it = 0; it < nkv; it++) {
