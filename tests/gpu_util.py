@@ -11,9 +11,10 @@ from workloads.inputs import bf16_round, rope_tables
 REL_L2_TOL = 1e-2      # relative L2 error of O against the oracle
 MAX_ABS_TOL = 3e-2     # max absolute error of O against the oracle
 # Absolute error of the natural-log normaliser against the oracle evaluated on the kernel's own
-# operand (kernel_q): the kernel sums the bf16-rounded weights into l, a relative error of at
-# most 2^-9 (ln(1 + 2^-9) = 1.95e-3), plus fp32 accumulation.
-LSE_ABS_TOL = 3e-3
+# operand (kernel_q): the kernel sums the bf16-rounded weights into l.  bf16 keeps 8 significant
+# bits, so each weight, and hence the sum, is off by a relative 2^-8 at most:
+# ln(1 + 2^-8) = 3.9e-3; 4e-3 with fp32 accumulation and the exp2/log2 approximations.
+LSE_ABS_TOL = 4e-3
 LN2 = math.log(2.0)
 
 

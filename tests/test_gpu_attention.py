@@ -181,3 +181,22 @@ def test_run_without_matching_plan_writes_nothing():
     assert (o == 7.0).all() and (lse == 3.0).all()
     with pytest.raises(ValueError):
         psa.run(q, k, v, grid, 128, psa.Workspace(1, 1, grid, 128, "cuda:0"))
+
+
+def test_layer_attention_follows_the_timestep_policy():
+    """Dense kernel during the exempt steps, the layer's single plan afterwards (same bits as the
+    direct calls)."""
+    from paper_2609_37001_amd.policy import LayerAttention, TimestepPolicy
+    torch = gu.torch()
+    f, hh, ww = 3, 8, 16
+    params = [(1, 0, INF, 2, 0, INF), (2, 1, 3, 1, 0, INF)]
+    q, k, v = (dev(x) for x in random_problem(1, 2, f * hh * ww, 128, seed=21))
+    layer = LayerAttention(params, (f, hh, ww), 128, 1, TimestepPolicy(10, 0.2), scale=0.1)
+    dense = psa.dense_fwd(q, k, v, 128, 0.1)
+    sparse = psa.attention_fwd(q, k, v, (f, hh, ww), 128, params, 0.1)
+    outs = [layer(q, k, v, step) for step in range(10)]
+    torch.cuda.synchronize()
+    ws = layer.workspace
+    assert all(torch.equal(o, dense) for o in outs[:2])
+    assert all(torch.equal(o, sparse) for o in outs[2:])
+    assert layer.workspace is ws

@@ -1,0 +1,95 @@
+"""Seeded random GPU parity cases: random grids (ragged ends, text), random stripe parameters
+from the paper's ranges, every (head_dim, block) variant, batch 1-2; 1D blocks and 3D PSABlocks.
+Every output row is compared with the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_37001_amd as psa
+from workloads.inputs import bf16_round
+
+import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+INF = 0x7FFFFFFF
+
+
+def dev(x):
+    t = gu.torch()
+    return t.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to("cuda:0").bfloat16()
+
+
+def random_params(rng, n, tmax, smax):
+    return [(int(rng.integers(1, tmax + 1)), int(rng.choice([0, 1, -1, 2, -2])), int(rng.choice([1, 2, 3, INF])),
+             int(rng.integers(1, smax + 1)), int(rng.choice([0, 1, -1])), int(rng.choice([1, 3, 5, 6, INF])))
+            for _ in range(n)]
+
+
+def compare(q, k, v, keep, scale, o, lse, block=1, groups=None):
+    num = den = mx = mlse = 0.0
+    for bi in range(q.shape[0]):
+        for hi in range(q.shape[1]):
+            o_ref, _ = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale, groups=groups)
+            _, l_ref = oracle.masked_attention(gu.kernel_q(q[bi, hi], scale), k[bi, hi], v[bi, hi], keep[hi], block,
+                                               gu.LN2, groups=groups)
+            og, lg = o[bi, hi].astype(np.float64), lse[bi, hi].astype(np.float64)
+            num += ((og - o_ref) ** 2).sum()
+            den += (o_ref ** 2).sum()
+            mx = max(mx, np.abs(og - o_ref).max())
+            fin = np.isfinite(l_ref)
+            assert (np.isneginf(lg) == ~fin).all() and (og[~fin] == 0).all()
+            if fin.any():
+                mlse = max(mlse, np.abs(lg[fin] - l_ref[fin]).max())
+    return (num / den) ** 0.5 if den > 0 else 0.0, mx, mlse
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_1d(seed):
+    rng = np.random.default_rng([7, seed])
+    d = int(rng.choice([64, 128]))
+    block = int(rng.choice([64, 128]))
+    f, hh, ww = int(rng.integers(1, 5)), int(rng.integers(1, 13)), int(rng.integers(1, 40))
+    nt = int(rng.choice([0, 0, int(rng.integers(1, 200))]))
+    n = f * hh * ww + nt
+    b, heads = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+    sp = -(-(hh * ww) // block)
+    params = random_params(rng, heads, f, sp)
+    scale = float(rng.uniform(0.05, 0.2))
+    q, k, v = (bf16_round(rng.standard_normal((b, heads, n, d)).astype(np.float32)) for _ in range(3))
+    o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, nt), block, params, scale, return_lse=True)
+    gu.torch().cuda.synchronize()
+    keep = oracle.blockmap(params, f, hh, ww, nt, block)
+    rel, mx, mlse = compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse.cpu().numpy(), block=block)
+    print("seed %d: n=%d d=%d block=%d rel %.2e max %.2e lse %.2e" % (seed, n, d, block, rel, mx, mlse))
+    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_3d(seed):
+    rng = np.random.default_rng([8, seed])
+    d = int(rng.choice([64, 128]))
+    tile = int(rng.choice([64, 128]))
+    shapes = [(1, 4, 16), (2, 4, 16), (1, 8, 16), (2, 8, 8), (3, 8, 16), (4, 4, 8), (1, 2, 64)]
+    pb = [s for s in shapes if (s[0] * s[1] * s[2]) % tile == 0][int(rng.integers(0, 3))]
+    f = int(rng.integers(1, 2 * pb[0] + 2))
+    hh = int(rng.integers(1, 2 * pb[1] + 3))
+    ww = int(rng.integers(1, 2 * pb[2] + 3))
+    nt = int(rng.choice([0, int(rng.integers(1, 100))]))
+    (tp, hp, wp), _ = oracle.psablock_grid(f, hh, ww, pb)
+    heads = int(rng.integers(1, 4))
+    params = random_params(rng, heads, tp, hp * wp)
+    scale = float(rng.uniform(0.05, 0.2))
+    n = f * hh * ww + nt
+    q, k, v = (bf16_round(rng.standard_normal((1, heads, n, d)).astype(np.float32)) for _ in range(3))
+    grid = (f, hh, ww, nt)
+    qb, kb, vb = (psa.to_blocks(dev(x), grid, pb) for x in (q, k, v))
+    ob, lseb = psa.attention_fwd_3d(qb, kb, vb, grid, pb, params, tile, scale, return_lse=True)
+    o = psa.from_blocks(ob, grid, pb)
+    gu.torch().cuda.synchronize()
+    lse = np.stack([oracle.from_blocks(lseb[0, h].cpu().numpy()[:, None], f, hh, ww, nt, pb)[:, 0]
+                    for h in range(heads)])[None]
+    keep = oracle.psablock_map(params, f, hh, ww, nt, pb)
+    groups = oracle.token_groups(f, hh, ww, nt, pb)
+    rel, mx, mlse = compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse, groups=groups)
+    print("seed %d: grid %s pb %s tile %d d %d rel %.2e max %.2e lse %.2e" % (seed, grid, pb, tile, d, rel, mx, mlse))
+    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
