@@ -33,7 +33,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA peak (published)
-KERNEL = "psa_sparse_kernel<128, 128>"
+KERNEL = "psa_sparse_kernel<128, 128, false>"
 COUNTERS_MD = os.path.join(ROOT, "profiles", "psa_sparse_kernel_wan14b_counters.md")
 SOURCES = ("paper_2609_37001_amd/csrc/psa_kernels.hip", "paper_2609_37001_amd/csrc/psa_launch.h",
            "paper_2609_37001_amd/csrc/psa_api.hip", "paper_2609_37001_amd/build.py", "include/psa.h")
@@ -71,6 +71,8 @@ def parse():
                    help="run one plain device copy of this many MiB first (counter calibration)")
     p.add_argument("--counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) and exit")
+    p.add_argument("--sweep-all", action="store_true",
+                   help="sparse at every forced density of the sweep workload against one dense run")
     p.add_argument("--search", type=int, default=0, metavar="K",
                    help="time PSA-Search scoring of K candidates per head (all heads per call)")
     p.add_argument("--kernel-stats", metavar="TRACE_DIR",
@@ -272,11 +274,13 @@ def cpu_baseline(cfg, params, seconds):
         n_blocks += 1
     elapsed = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    full = 4.0 * cfg.head_dim * cfg.batch * float((bmap * lens[None, :, None] * lens[None, None, :]).sum())
     return {
         "value": flops / elapsed / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
+        "extrapolated_full_step_s": round(full / (flops / elapsed), 1),
         "sample": "%d query blocks of 128 rows from heads %s of the same workload (float64 numpy "
                   "oracle, %.1f s, %d host cores visible); %.3g TFLOP computed, mean %.1f kept "
                   "blocks per sampled row" % (n_blocks, sorted(int(x) for x in heads), elapsed,
@@ -441,6 +445,42 @@ def bench_search(args, cfg, torch, psa):
     return 0
 
 
+def bench_sweep(args, torch, psa):
+    """Every density of the sweep workload (the Wan 14B shape), sparse against one dense run."""
+    from workloads import get_config, make_qkv, stripe_params
+    from workloads.configs import SWEEP_TARGETS
+    cfg = get_config("sweep")
+    grid = (cfg.frames, cfg.height, cfg.width, cfg.n_text)
+    q, k, v = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to("cuda:0")
+               for x in make_qkv(cfg, workers=16))
+    o = torch.empty_like(q)
+    ws = psa.Workspace(cfg.batch, cfg.heads, grid, cfg.block, q.device)
+    dms = time_calls(lambda: psa.dense_fwd(q, k, v, cfg.block, cfg.scale, out=o), 4, 1, torch)["mean"]
+    rows = []
+    for target in SWEEP_TARGETS:
+        params = stripe_params("sweep", target)
+        flops, density = computed_flops(psa, cfg, params, torch)
+        t = time_calls(lambda: psa.attention_fwd(q, k, v, grid, cfg.block, params, cfg.scale, out=o,
+                                                 workspace=ws), args.steps, args.warmup, torch)
+        tf = flops / (t["mean"] * 1e-3) / 1e12
+        rows.append({"target": target, "density": round(density, 4), "ms": round(t["mean"], 3),
+                     "tflops": round(tf, 1), "speedup_vs_dense": round(dms / t["mean"], 3),
+                     "speedup_x_density": round(dms / t["mean"] * density, 3)})
+        log("sweep %.2f: density %.4f, %.3f ms, %.1f TFLOP/s, speedup %.2f (x density %.3f)"
+            % (target, density, t["mean"], tf, dms / t["mean"], dms / t["mean"] * density))
+    best = max(rows, key=lambda r: r["tflops"])
+    result = {
+        "metric": "sparse-attn fwd computed TFLOP/s & MFU; speedup vs own dense at Wan-14B shape",
+        "value": rows[3]["tflops"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": rows[3]["ms"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT["sweep"] + "; value is the 30 % run, every run below"},
+        "dense_ms": round(dms, 3), "sweep": rows, "best_tflops": best["tflops"],
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.kernel_stats:
@@ -469,6 +509,8 @@ def main():
         return bench_3d(args, cfg, params, torch, psa)
     if args.search:
         return bench_search(args, cfg, torch, psa)
+    if args.sweep_all:
+        return bench_sweep(args, torch, psa)
     grid = (cfg.frames, cfg.height, cfg.width, cfg.n_text)
     log("workload %s: generating inputs" % name)
     t0 = time.perf_counter()
