@@ -108,6 +108,13 @@ def _grid_tuple(grid):
     return g + (0,) if len(g) == 3 else g
 
 
+def _check_tokens(n, grid):
+    """The library sees raw pointers: a tensor shorter than the grid would be read past its end."""
+    f, h, w, nt = _grid_tuple(grid)
+    if n != f * h * w + nt:
+        raise ValueError("tensors hold %d tokens, the grid %s has %d" % (n, (f, h, w, nt), f * h * w + nt))
+
+
 def build_blockmap(params, grid, block, device=None, blockmap=True, per_row=True, per_head=True,
                    stream=None):
     """Block map of the stripe parameters on the device.
@@ -139,6 +146,7 @@ def attention_fwd(q, k, v, grid, block, params, scale=None, out=None, return_lse
     b, h, n, d = q.shape
     if len(params) != h:
         raise ValueError("one stripe tuple per head is required")
+    _check_tokens(n, grid)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     o = torch.empty_like(q) if out is None else out
     _check_qkv(q, o)
@@ -190,6 +198,7 @@ def run(q, k, v, grid, block, workspace, scale=None, out=None, return_lse=False,
     o = torch.empty_like(q) if out is None else out
     _check_qkv(q, o)
     lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+    _check_tokens(n, grid)
     ws = workspace
     if ws.params is None:
         raise ValueError("the workspace holds no plan: call plan() or attention_fwd() first")
