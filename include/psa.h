@@ -123,9 +123,10 @@ psa_status_t psa_attention_plan(int32_t batch, int32_t n_heads, psa_grid_t grid,
  * (Algorithm 1) and run the tile engine over them.  Arguments as in psa_attention_fwd.  The
  * workspace must hold a plan made for the same batch, n_heads, grid and block; the kernel checks
  * the plan's header first and, on a mismatch or an unfinished plan, writes nothing (o and lse keep
- * their contents; no error can be returned for a condition found on the device).  The run uses
- * the plan's queue counters and re-arms them before it ends, so runs over one workspace must not
- * overlap in time (use one workspace per stream). */
+ * their contents; no error can be returned for a condition found on the device).  The run
+ * re-arms the plan's queue counters (a one-thread kernel ahead of the attention kernel) and
+ * consumes them, so runs over one workspace must not overlap in time (use one workspace per
+ * stream). */
 psa_status_t psa_attention_run(const void* q, const void* k, const void* v, void* o,
                                int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
                                int32_t block, float softmax_scale, void* workspace,

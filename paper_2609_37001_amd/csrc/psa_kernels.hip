@@ -515,8 +515,7 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
     for (int32_t qb = lo; qb < hi; qb++) dst[qb - lo] = item0 + qb;
   }
   if (tid <= kNumQueues) queues[tid] = qstart[tid];
-  if (tid < kNumQueues) queues[kQueueCounters + tid] = 0;
-  if (tid == 0) queues[kQueueDone] = 0;
+  if (tid < kNumQueues) queues[kQueueCounters + tid * kCounterStride] = 0;
   __syncthreads();
   if (tid == 0) {
     __threadfence();
@@ -954,6 +953,23 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
   }
 }
 
+// Whether a workspace holds a finished plan for exactly the sizes of this launch.
+__device__ __forceinline__ bool plan_matches(const PlanHeader& h, const PlanHeader& e) {
+  return h.magic == kPlanMagic && h.n_bh == e.n_bh && h.n_heads == e.n_heads && h.nb == e.nb &&
+         h.block == e.block && h.n == e.n && h.frames == e.frames && h.height == e.height &&
+         h.width == e.width && h.n_text == e.n_text && h.pbt == e.pbt && h.pbh == e.pbh &&
+         h.pbw == e.pbw;
+}
+
+// Re-arms the plan's queue counters before each run (a workspace without a matching plan is
+// left alone).
+__global__ __launch_bounds__(64) void psa_rearm_kernel(int32_t* __restrict__ queues,
+                                                       const PlanHeader* __restrict__ header,
+                                                       PlanHeader expect) {
+  if (!plan_matches(*header, expect)) return;
+  if (threadIdx.x < kNumQueues) queues[kQueueCounters + threadIdx.x * kCounterStride] = 0;
+}
+
 // Persistent sparse attention (two 4-wave workgroups per CU).  Workgroup w starts on queue w % kNumQueues (its XCD under
 // round-robin dispatch) and moves on to the next queue when one runs dry, so every workgroup
 // exits once all queues are exhausted.
@@ -972,13 +988,7 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 
   // A workspace without a finished plan for exactly these sizes is left alone: nothing is read
   // through its queues and no output is written.
-  const PlanHeader h = *header;
-  if (h.magic != kPlanMagic || h.n_bh != expect.n_bh || h.n_heads != expect.n_heads ||
-      h.nb != expect.nb || h.block != expect.block || h.n != expect.n ||
-      h.frames != expect.frames || h.height != expect.height || h.width != expect.width ||
-      h.n_text != expect.n_text || h.pbt != expect.pbt || h.pbh != expect.pbh ||
-      h.pbw != expect.pbw)
-    return;
+  if (!plan_matches(*header, expect)) return;
   const int32_t n_heads = expect.n_heads, n = expect.n, nb = expect.nb;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -990,7 +1000,12 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
       int32_t item = -1;
       while (exhausted < kNumQueues) {
         const int32_t start = queues[queue], len = queues[queue + 1] - start;
-        const int32_t idx = atomicAdd(&queues[kQueueCounters + queue], 1);
+        int32_t* ctr = &queues[kQueueCounters + queue * kCounterStride];
+        // Counters only grow: a value at or past the end is final, so an exhausted queue is
+        // recognised with a load and costs no atomic.
+        int32_t idx = len;
+        if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < len)
+          idx = atomicAdd(ctr, 1);
         if (idx < len) {
           item = order[start + idx];
           break;
@@ -1002,18 +1017,7 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
     __syncthreads();
     const int32_t item = misc[7];
-    if (item < 0) {
-      // The last workgroup out re-arms the counters, so the plan serves the next run as is.
-      if (tid == 0) {
-        __threadfence();
-        if (atomicAdd(&queues[kQueueDone], 1) == (int32_t)gridDim.x - 1) {
-          __threadfence();
-          for (int x = 0; x < kNumQueues; x++) atomicExch(&queues[kQueueCounters + x], 0);
-          atomicExch(&queues[kQueueDone], 0);
-        }
-      }
-      break;
-    }
+    if (item < 0) break;
     const int32_t bh = item / nb, qb = item - bh * nb;
     const psa_stripe_t m = params[bh % n_heads];
 
@@ -1076,6 +1080,10 @@ static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, v
                                   void* workspace, const WorkspaceLayout& wl, int32_t n_wg,
                                   hipStream_t stream) {
   char* ws = (char*)workspace;
+  hipLaunchKernelGGL(psa_rearm_kernel, dim3(1), dim3(64), 0, stream, (int32_t*)(ws + wl.queues),
+                     (const PlanHeader*)(ws + wl.header), expect);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((psa_sparse_kernel<D, BLK, PAD>), dim3(n_wg), dim3(Tile<D, BLK>::kThreads), 0, stream,
                      (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
                      (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),

@@ -56,11 +56,12 @@ struct PlanHeader {
   int32_t pbt, pbh, pbw;
 };
 
-// Layout of the queue area: kNumQueues + 1 boundaries, kNumQueues pop counters, one exit
-// counter.
-constexpr int kQueueCounters = kNumQueues + 1;
-constexpr int kQueueDone = 2 * kNumQueues + 1;
-constexpr int kQueueWords = 2 * kNumQueues + 2;
+// Layout of the queue area (int32 words): kNumQueues + 1 boundaries in the first 128-byte line,
+// then one pop counter per queue, each in a line of its own (device-scope atomics on one line
+// are serialised).
+constexpr int kCounterStride = 32;
+constexpr int kQueueCounters = 32;
+constexpr int kQueueWords = kQueueCounters + kNumQueues * kCounterStride;
 
 // Workspace of psa_attention_plan / psa_attention_run (byte offsets, each 256-aligned).
 struct WorkspaceLayout {
@@ -69,7 +70,7 @@ struct WorkspaceLayout {
   size_t coords;    // int2 [nb]: (frame, slot) of each block, frame = -1 for a global block
   size_t counts;    // int32 [batch*n_heads*nb]: kept key blocks per work item
   size_t order;     // int32 [batch*n_heads*nb]: work items in schedule order
-  size_t queues;    // int32 [kQueueWords]: queue boundaries, pop counters, exit counter
+  size_t queues;    // int32 [kQueueWords]: queue boundaries and pop counters
   size_t masks;     // uint64 [nb][2]: valid positions of each tile (3D only)
   size_t total;
 };
