@@ -425,31 +425,90 @@ __global__ __launch_bounds__(256) void psa_count_kernel(const psa_stripe_t* __re
 // decoding the list and the epilogue.
 constexpr int kItemOverhead = 2;
 
-// Single workgroup.  Orders the (batch, head) pairs by total work, longest first, and cuts every
-// head's query blocks into kNumQueues contiguous ranges of equal work; queue x (the XCD of the
-// workgroups that start on it) lists range x of every head in that order.  All XCDs therefore
-// sweep the heads together -- the K/V of the one or two heads in flight stay in the memory-side
-// cache -- and the workgroups of one XCD stream neighbouring key blocks through its L2.
+// An item whose work exceeds kLongFactor times the mean item work is scheduled ahead of all
+// others (for example the rows of the global text tokens, which keep every key block): taken
+// late, one such item would still run long after the rest of the device has drained.
+constexpr int kLongFactor = 3;
+// Long items are sorted into this many classes of equal width in [0, max work].
+constexpr int kWorkClasses = 64;
+constexpr int kScheduleWaves = 16;
+
+// Single workgroup.  Every queue x (the XCD of the workgroups that start on it) begins with its
+// share of the long items, longest first and dealt round-robin over the queues.  The other items
+// follow head by head: the (batch, head) pairs are ordered by their work, longest first, and
+// every head's query blocks are cut into kNumQueues contiguous ranges of equal work, queue x
+// listing range x of every head.  All XCDs therefore sweep the heads together -- the K/V of the
+// one or two heads in flight stay in the memory-side cache -- and the workgroups of one XCD
+// stream neighbouring key blocks through its L2.
 __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __restrict__ counts,
                                                             int32_t* __restrict__ order,
                                                             int32_t* __restrict__ queues,
                                                             PlanHeader* __restrict__ header,
                                                             PlanHeader done, int32_t nb) {
-  const int32_t n_bh = done.n_bh;
+  const int32_t n_bh = done.n_bh, n = n_bh * nb;
   __shared__ int64_t total[PSA_MAX_BATCH_HEADS];
   __shared__ int32_t by_rank[PSA_MAX_BATCH_HEADS];
   __shared__ uint16_t bounds[PSA_MAX_BATCH_HEADS][kNumQueues + 1];
   __shared__ int32_t qoff[PSA_MAX_BATCH_HEADS][kNumQueues];
+  __shared__ int32_t hist[kScheduleWaves][kWorkClasses];
   __shared__ int32_t qstart[kNumQueues + 1];
+  __shared__ uint64_t all_work;
+  __shared__ int32_t max_count, n_long;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
 
-  for (int32_t bh = wave; bh < n_bh; bh += 16) {
+  if (tid == 0) {
+    all_work = 0;
+    max_count = 0;
+  }
+  for (int32_t i = tid; i < kScheduleWaves * kWorkClasses; i += 1024) (&hist[0][0])[i] = 0;
+  __syncthreads();
+  constexpr int kLoads = 4;                 // loads in flight per lane in the sweeps below
+  for (int32_t bh = wave; bh < n_bh; bh += kScheduleWaves) {
     int64_t s = 0;
-    for (int32_t qb = lane; qb < nb; qb += 64) s += counts[(int64_t)bh * nb + qb] + kItemOverhead;
-    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-    if (lane == 0) total[bh] = s;
+    int32_t mx = 0;
+    for (int32_t q0 = lane; q0 < nb; q0 += 64 * kLoads) {
+      int32_t c[kLoads];
+#pragma unroll
+      for (int j = 0; j < kLoads; j++) c[j] = q0 + 64 * j < nb ? counts[bh * nb + q0 + 64 * j] : -1;
+#pragma unroll
+      for (int j = 0; j < kLoads; j++) {
+        s += c[j] < 0 ? 0 : c[j] + kItemOverhead;
+        mx = max(mx, c[j]);
+      }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+      s += __shfl_xor(s, off);
+      mx = max(mx, __shfl_xor(mx, off));
+    }
+    if (lane == 0) {
+      total[bh] = s;
+      atomicAdd(&all_work, (uint64_t)s);
+      atomicMax(&max_count, mx);
+    }
   }
   __syncthreads();
+  const int64_t long_above = (int64_t)kLongFactor * (int64_t)all_work;
+  auto work_of = [&](int32_t item) { return (int64_t)counts[item] + kItemOverhead; };
+  // Whether any item is long follows from the largest one; without long items every pass that
+  // looks for them is skipped.
+  const bool any_long = ((int64_t)max_count + kItemOverhead) * n > long_above;
+  auto is_long = [&](int32_t item) { return any_long && work_of(item) * n > long_above; };
+  if (any_long) {
+    // Work of each pair without its long items.
+    for (int32_t bh = wave; bh < n_bh; bh += kScheduleWaves) {
+      int64_t s = 0;
+      for (int32_t q0 = lane; q0 < nb; q0 += 64 * kLoads) {
+        int64_t w[kLoads];
+#pragma unroll
+        for (int j = 0; j < kLoads; j++) w[j] = q0 + 64 * j < nb ? work_of(bh * nb + q0 + 64 * j) : 0;
+#pragma unroll
+        for (int j = 0; j < kLoads; j++) s += w[j] * n > long_above ? 0 : w[j];
+      }
+      for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+      if (lane == 0) total[bh] = s;
+    }
+    __syncthreads();
+  }
   for (int32_t bh = tid; bh < n_bh; bh += 1024) {
     int32_t r = 0;
     const int64_t mine = total[bh];
@@ -458,45 +517,103 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
   }
   __syncthreads();
 
-  // Equal-work ranges of each head: bounds[r][x] = first query block of range x.
-  for (int32_t r = wave; r < n_bh; r += 16) {
+  // Equal-work ranges of each head over its other items: bounds[r][x] = first query block of
+  // range x.
+  for (int32_t r = wave; r < n_bh; r += kScheduleWaves) {
     const int32_t bh = by_rank[r];
     const int64_t head_total = total[bh];
     int64_t base = 0;
     int32_t next = 1;                       // next boundary to place
     if (lane == 0) bounds[r][0] = 0;
-    for (int32_t q0 = 0; q0 < nb && next < kNumQueues; q0 += 64) {
-      const int32_t qb = q0 + lane;
-      int64_t w = qb < nb ? counts[(int64_t)bh * nb + qb] + kItemOverhead : 0;
-      int64_t incl = w;                     // inclusive prefix over the wave
-      for (int off = 1; off < 64; off <<= 1) {
-        const int64_t t = __shfl_up(incl, off);
-        if (lane >= off) incl += t;
+    for (int32_t g0 = 0; g0 < nb && next < kNumQueues; g0 += 64 * kLoads) {
+      int64_t wv[kLoads];
+#pragma unroll
+      for (int j = 0; j < kLoads; j++) {
+        const int32_t qb = g0 + 64 * j + lane;
+        wv[j] = qb < nb && !is_long(bh * nb + qb) ? work_of(bh * nb + qb) : 0;
       }
-      const int64_t excl = base + incl - w;
-      // range x starts at the first block whose preceding work reaches x/Q of the head
-      while (next < kNumQueues) {
-        const int64_t target = head_total * next / kNumQueues;
-        const uint64_t hit = __builtin_amdgcn_ballot_w64(qb < nb && excl >= target);
-        if (!hit) break;
-        const int32_t first = q0 + __builtin_ctzll(hit);
-        if (lane == 0) bounds[r][next] = (uint16_t)first;
-        next++;
+#pragma unroll
+      for (int j = 0; j < kLoads; j++) {
+        const int32_t q0 = g0 + 64 * j, qb = q0 + lane;
+        const int64_t w = wv[j];
+        int64_t incl = w;                   // inclusive prefix over the wave
+        for (int off = 1; off < 64; off <<= 1) {
+          const int64_t t = __shfl_up(incl, off);
+          if (lane >= off) incl += t;
+        }
+        const int64_t excl = base + incl - w;
+        // range x starts at the first block whose preceding work reaches x/Q of the head
+        while (next < kNumQueues) {
+          const int64_t target = head_total * next / kNumQueues;
+          const uint64_t hit = __builtin_amdgcn_ballot_w64(qb < nb && excl >= target);
+          if (!hit) break;
+          const int32_t first = q0 + __builtin_ctzll(hit);
+          if (lane == 0) bounds[r][next] = (uint16_t)first;
+          next++;
+        }
+        base += __shfl(incl, 63);
       }
-      base += __shfl(incl, 63);
     }
     for (; next < kNumQueues; next++)
       if (lane == 0) bounds[r][next] = (uint16_t)nb;
     if (lane == 0) bounds[r][kNumQueues] = (uint16_t)nb;
   }
+
+  // Long items: stable class sort.  Entry s of the unsorted list is query block s mod nb of the
+  // pair of rank s div nb; wave w owns the slice [w n / W, (w + 1) n / W).  Class 0 holds the
+  // longest items.
+  const int32_t lo = (int32_t)((int64_t)n * wave / kScheduleWaves);
+  const int32_t hi = (int32_t)((int64_t)n * (wave + 1) / kScheduleWaves);
+  const int32_t top = max_count + 1;
+  auto item_of = [&](int32_t s) { const int32_t r = s / nb; return by_rank[r] * nb + (s - r * nb); };
+  auto class_of = [&](int32_t item) {
+    return kWorkClasses - 1 - (int32_t)((int64_t)counts[item] * kWorkClasses / top);
+  };
+  if (any_long)
+    for (int32_t s = lo + lane; s < hi; s += 64) {
+      const int32_t item = item_of(s);
+      if (is_long(item)) atomicAdd(&hist[wave][class_of(item)], 1);
+    }
   __syncthreads();
 
-  // Offsets of each head's range inside its queue, and the queue starts.
+  // Number of the other items in every (head, queue) range, one wave per range.
+  for (int32_t pair = wave; pair < n_bh * kNumQueues; pair += kScheduleWaves) {
+    const int32_t r = pair / kNumQueues, x = pair - r * kNumQueues;
+    const int32_t item0 = by_rank[r] * nb, end = bounds[r][x + 1];
+    int32_t c = end - bounds[r][x];
+    if (any_long)
+      for (int32_t qb = bounds[r][x] + lane; __builtin_amdgcn_readfirstlane(qb - lane) < end; qb += 64)
+        c -= __builtin_popcountll(__builtin_amdgcn_ballot_w64(qb < end && is_long(item0 + qb)));
+    if (lane == 0) qoff[r][x] = c;
+  }
+  // Exclusive scan of the class histogram in (class, wave) order: hist[w][c] becomes the first
+  // list position of the class-c long items of slice w.
+  if (wave == 0) {
+    int32_t col = 0;
+    for (int w = 0; w < kScheduleWaves; w++) col += hist[w][lane];
+    int32_t incl = col;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t t = __shfl_up(incl, off);
+      if (lane >= off) incl += t;
+    }
+    int32_t pos = incl - col;
+    for (int w = 0; w < kScheduleWaves; w++) {
+      const int32_t h = hist[w][lane];
+      hist[w][lane] = pos;
+      pos += h;
+    }
+    if (lane == 63) n_long = incl;
+  }
+  __syncthreads();
+  // Offsets of each head's range inside its queue, and the queue starts: queue x holds long
+  // list positions x, x + Q, ... (n_long div Q of them, one more for x < n_long mod Q), then
+  // its ranges.
   if (tid < kNumQueues) {
-    int32_t acc = 0;
+    int32_t acc = n_long / kNumQueues + (tid < n_long % kNumQueues ? 1 : 0);
     for (int32_t r = 0; r < n_bh; r++) {
+      const int32_t c = qoff[r][tid];
       qoff[r][tid] = acc;
-      acc += bounds[r][tid + 1] - bounds[r][tid];
+      acc += c;
     }
     qstart[tid + 1] = acc;                  // length, turned into a start below
   }
@@ -507,12 +624,39 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
   }
   __syncthreads();
 
-  for (int32_t pair = tid; pair < n_bh * kNumQueues; pair += 1024) {
+  // Stable scatter of the long items: the lanes of one 64-entry chunk that share a class are
+  // found with one ballot per class bit; each takes the next position of its class in the order
+  // of its lane.
+  for (int32_t s0 = lo; any_long && s0 < hi; s0 += 64) {
+    const int32_t s = s0 + lane;
+    const int32_t item = s < hi ? item_of(s) : 0;
+    const bool valid = s < hi && is_long(item);
+    if (!__builtin_amdgcn_ballot_w64(valid)) continue;
+    const int32_t cls = valid ? class_of(item) : 0;
+    uint64_t same = __builtin_amdgcn_ballot_w64(valid);
+    for (int bit = 1; bit < kWorkClasses; bit <<= 1) {
+      const uint64_t ones = __builtin_amdgcn_ballot_w64(valid && (cls & bit));
+      same &= (cls & bit) ? ones : ~ones;
+    }
+    const int32_t base = valid ? hist[wave][cls] : 0;
+    __builtin_amdgcn_wave_barrier();
+    if (valid) {
+      const int32_t pos = base + __builtin_popcountll(same & ((1ull << lane) - 1));
+      order[qstart[pos % kNumQueues] + pos / kNumQueues] = item;
+      if (__builtin_ctzll(same) == lane) hist[wave][cls] = base + __builtin_popcountll(same);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  for (int32_t pair = wave; pair < n_bh * kNumQueues; pair += kScheduleWaves) {
     const int32_t r = pair / kNumQueues, x = pair - r * kNumQueues;
-    const int32_t item0 = by_rank[r] * nb;
+    const int32_t item0 = by_rank[r] * nb, end = bounds[r][x + 1];
     int32_t* dst = order + qstart[x] + qoff[r][x];
-    const int32_t lo = bounds[r][x], hi = bounds[r][x + 1];
-    for (int32_t qb = lo; qb < hi; qb++) dst[qb - lo] = item0 + qb;
+    for (int32_t qb = bounds[r][x] + lane; __builtin_amdgcn_readfirstlane(qb - lane) < end; qb += 64) {
+      const bool keep = qb < end && !is_long(item0 + qb);
+      const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
+      if (keep) dst[__builtin_popcountll(mask & ((1ull << lane) - 1))] = item0 + qb;
+      dst += __builtin_popcountll(mask);
+    }
   }
   if (tid <= kNumQueues) queues[tid] = qstart[tid];
   if (tid < kNumQueues) queues[kQueueCounters + tid * kCounterStride] = 0;

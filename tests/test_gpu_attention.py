@@ -80,6 +80,24 @@ def test_shapes_ragged_text_batch(d, block):
     assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
 
 
+def test_long_text_rows_scheduled_first():
+    """Text rows keep every key block while the video rows keep one block plus the text: the
+    text rows' work is far above three times the mean, so the plan lists them ahead of the
+    head-ordered ranges.  Batch 2 x 6 heads x 3 text blocks = 36 such items over 8 queues."""
+    f, hh, ww, nt = 8, 16, 32, 300
+    n = f * hh * ww + nt
+    params = [(1, 0, INF, 1, 0, INF)] * 4 + [(1, 1, INF, 1, 0, INF), (2, 0, INF, 1, 0, INF)]
+    q, k, v = random_problem(2, len(params), n, 64, seed=23)
+    keep = oracle.blockmap(params, f, hh, ww, nt, 128)
+    rows = oracle.kept_per_row(keep) + 2
+    assert (rows[:, -3:] * rows.size > 3 * rows.sum()).all() and (rows[:, :-3] * rows.size <= 3 * rows.sum()).all()
+    o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, nt), 128, params, 0.1, return_lse=True)
+    gu.torch().cuda.synchronize()
+    rel, mx, mlse = full_compare(q, k, v, keep, 128, 0.1, o, lse)
+    print("long text rows: rel_l2 %.2e max_abs %.2e lse %.2e" % (rel, mx, mlse))
+    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+
+
 @pytest.mark.parametrize("d,block", [(64, 64), (128, 128)])
 def test_dense_full(d, block):
     n = 3 * block + 29
