@@ -33,6 +33,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA peak (published)
+HBM_PEAK = 8.0e12             # MI355X HBM3E bandwidth, bytes/s (published)
 KERNEL = "psa_sparse_kernel<128, 128, false>"
 COUNTERS_MD = os.path.join(ROOT, "profiles", "psa_sparse_kernel_wan14b_counters.md")
 SOURCES = ("paper_2609_37001_amd/csrc/psa_kernels.hip", "paper_2609_37001_amd/csrc/psa_launch.h",
@@ -71,6 +72,13 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--copy-mb", type=int, default=0,
                    help="run one plain device copy of this many MiB first (counter calibration)")
+    p.add_argument("--waits", metavar="PMC_DIR",
+                   help="wave-cycle breakdown of the attention kernels from a rocprofv3 --pmc run of "
+                        "SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY "
+                        "SQ_ACTIVE_INST_MISC SQ_ACTIVE_INST_SCA GRBM_GUI_ACTIVE, and exit")
+    p.add_argument("--hbm", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "TRACE_DIR"),
+                   help="HBM bytes and bandwidth of the sparse and dense kernels of --workload from "
+                        "two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) and a kernel trace, and exit")
     p.add_argument("--counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) and exit")
     p.add_argument("--sweep-all", action="store_true",
@@ -218,6 +226,70 @@ def utilisation_rows(sq_dir, tcc_dir, trace_dir, label):
             a["SQ_ACTIVE_INST_VALU"] * 4 / (cyc * 1024), a["SQ_LDS_BANK_CONFLICT"],
             b["TCC_HIT_sum"] / (b["TCC_HIT_sum"] + b["TCC_MISS_sum"])))
     return rows
+
+
+def hbm_rows(fetch_dir, write_dir, trace_dir, cfg, copy_mb):
+    """HBM-side bytes and bandwidth of the attention kernels: FETCH_SIZE and WRITE_SIZE per
+    dispatch, each scaled by what it reads for the plain 'copy_mb' MiB device copy of the same
+    run, over the kernel's average duration in the trace."""
+    fetch, write = counter_rows(fetch_dir, "FETCH_SIZE"), counter_rows(write_dir, "WRITE_SIZE")
+    copy_bytes = copy_mb * 1048576.0
+
+    def scale(rows):
+        copies = [max(v) for k, v in rows.items() if "copyBuffer" in k]
+        if not copies:
+            raise SystemExit("no copy dispatch in %s: profile it with --copy-mb" % rows)
+        return copy_bytes / (copies[0] * 1024.0)
+
+    f_scale, w_scale = scale(fetch), scale(write)
+    dur = {}
+    for path in glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                dur[r["Name"].split("(")[0].replace("void ", "").replace("psa::", "")] = float(r["AverageNs"]) * 1e-9
+    algo = 8.0 * cfg.batch * cfg.heads * cfg.n_tokens * cfg.head_dim
+    rows = []
+    for full, vals in sorted(fetch.items()):
+        k = full.split("(")[0].replace("void ", "").replace("psa::", "")
+        if not k.startswith(("psa_sparse", "psa_dense")):
+            continue
+        wv = [v for kk, v in write.items() if kk.split("(")[0].replace("void ", "").replace("psa::", "") == k][0]
+        rd = sum(vals) / len(vals) * 1024.0 * f_scale
+        wr = sum(wv) / len(wv) * 1024.0 * w_scale
+        t = dur[k]
+        rows.append("| %s | %s | %.2f | %.1f | %.3f | %.3f | %.0f | %.3f |" % (
+            cfg.name, k, t * 1e3, rd / 1e9, wr / 1e9, algo / 1e9, (rd + wr) / t / 1e9, (rd + wr) / t / HBM_PEAK))
+    return rows
+
+
+HBM_HEADER = ("| workload | kernel | ms (trace) | read GB | written GB | algorithmic GB | achieved GB/s | "
+              "fraction of 8 TB/s |\n|---|---|---|---|---|---|---|---|")
+
+
+def wait_rows(run_dir, label):
+    """Where the waves of the attention kernels spend their cycles: executing, waiting for a
+    dependency (data, waitcnt, barrier), or ready but waiting for the issue port (per-wave
+    quad-cycle counters over SQ_WAVE_CYCLES)."""
+    out = {}
+    for path in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                name = r["Kernel_Name"].split("(")[0].replace("void ", "").replace("psa::", "")
+                if name.startswith(("psa_sparse", "psa_dense")):
+                    out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    rows = []
+    for k in sorted(out):
+        m = {c: sum(v) / len(v) for c, v in out[k].items()}
+        wave = m["SQ_WAVE_CYCLES"]
+        rows.append("| %s | %s | %.2f | %.3f | %.3f | %.3f | %.3f | %.3f |" % (
+            label, k, wave * 4 / (m["GRBM_GUI_ACTIVE"] / 8.0 * 1024), m["SQ_ACTIVE_INST_ANY"] / wave,
+            m["SQ_WAIT_ANY"] / wave, m["SQ_WAIT_INST_ANY"] / wave, m["SQ_ACTIVE_INST_SCA"] / wave,
+            m["SQ_ACTIVE_INST_MISC"] / wave))
+    return rows
+
+
+WAIT_HEADER = ("| workload | kernel | waves per SIMD | executing | waiting for a dependency | "
+               "waiting for issue | scalar | branch |\n|---|---|---|---|---|---|---|---|")
 
 
 UTIL_HEADER = ("| workload | kernel | ms (trace) | clock GHz | MFMA busy | MFMA cycles per MFMA | "
@@ -495,6 +567,15 @@ def main():
         return 0
     if args.counters:
         sys.stdout.write(summarise_counters(args.counters[0], args.counters[1], args.copy_calibration_mb))
+        return 0
+    if args.waits:
+        print(WAIT_HEADER)
+        print("\n".join(wait_rows(args.waits, os.path.basename(os.path.normpath(args.waits)))))
+        return 0
+    if args.hbm:
+        from workloads import get_config
+        print(HBM_HEADER)
+        print("\n".join(hbm_rows(*args.hbm, get_config(args.workload), args.copy_calibration_mb)))
         return 0
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the attention "

@@ -70,6 +70,34 @@ def test_kernel_table_and_utilisation(tmp_path):
     assert cells[2:6] == ["100.00", "1.90", "0.500", "32.0"] and cells[-1] == "0.900"
 
 
+def test_hbm_and_wait_summaries(tmp_path):
+    trace = tmp_path / "t"
+    os.makedirs(trace)
+    with open(trace / "run_kernel_stats.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs",
+                                          "MaxNs"])
+        w.writeheader()
+        w.writerow({"Name": "void psa::psa_sparse_kernel<128, 128, false>(x)", "Calls": 1, "TotalDurationNs": 1e7,
+                    "AverageNs": 1e7, "Percentage": 100.0, "MinNs": 1e7, "MaxNs": 1e7})
+    k = "void psa::psa_sparse_kernel<128, 128, false>(x)"
+    write_counters(tmp_path / "f", [("__amd_rocclr_copyBuffer", "FETCH_SIZE", 524288), (k, "FETCH_SIZE", 1e6)])
+    write_counters(tmp_path / "w", [("__amd_rocclr_copyBuffer", "WRITE_SIZE", 1048576), (k, "WRITE_SIZE", 1e4)])
+    cfg = get_config("tiny")
+    row = bench.hbm_rows(str(tmp_path / "f"), str(tmp_path / "w"), str(trace), cfg, 1024)[0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    rd, wr = 1e6 * 1024 * 2, 1e4 * 1024            # fetch scale 2, write scale 1
+    assert cells[0] == "tiny" and cells[2] == "10.00"
+    assert float(cells[3]) == round(rd / 1e9, 1) and float(cells[4]) == round(wr / 1e9, 3)
+    assert float(cells[5]) == round(4 * 2 * (2 * 1024 * 64) / 1e9, 3)   # Q, K, V, O: 2 B x 2 heads x N x d
+    assert float(cells[6]) == round((rd + wr) / 1e-2 / 1e9)
+    write_counters(tmp_path / "q", [(k, "GRBM_GUI_ACTIVE", 8 * 1000.0), (k, "SQ_WAVE_CYCLES", 512 * 1000.0),
+                                    (k, "SQ_ACTIVE_INST_ANY", 512 * 300.0), (k, "SQ_WAIT_ANY", 512 * 400.0),
+                                    (k, "SQ_WAIT_INST_ANY", 512 * 300.0), (k, "SQ_ACTIVE_INST_SCA", 512 * 50.0),
+                                    (k, "SQ_ACTIVE_INST_MISC", 512 * 10.0)])
+    cells = [c.strip() for c in bench.wait_rows(str(tmp_path / "q"), "x")[0].strip("|").split("|")]
+    assert cells[2:] == ["2.00", "0.300", "0.400", "0.300", "0.050", "0.010"]
+
+
 def test_group_tokens_of_the_psablock_workload():
     cfg = get_config("wan14b_3d")
     cnt = bench.group_tokens(cfg)
