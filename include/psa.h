@@ -105,8 +105,10 @@ psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa
 
 /* Plan of psa_attention_run (the work list of Algorithm 2 without the attention itself): copies
  * the stripe parameters of each head to the workspace, counts the kept key blocks of every
- * (batch, head, query block) work item with the Algorithm 1 decoder, orders the items longest
- * head first and splits each head into equal-work ranges, one work queue per XCD.  The plan
+ * (batch, head, query block) work item with the Algorithm 1 decoder and orders the items: those
+ * of more than three times the mean work (rows that keep every key block, such as text rows)
+ * first, longest first, then the heads longest first, each split into equal-work ranges, one
+ * work queue per XCD.  The plan
  * depends only on the sizes and on params, so one plan serves any number of runs (a layer's
  * stripes stay fixed over the denoising steps).
  *   workspace     device, psa_workspace_size(batch, n_heads, grid, block) bytes or more,
