@@ -864,14 +864,23 @@ __device__ __forceinline__ void qk_half(const WaveState<D, BLK>& st,
   const int h = lane >> 5;
   const int krow0 = k0 + key_perm(lane & 31);
   const int ksw = swz<T::CPR>(krow0);   // identical for krow0 + 32 kt
+  // The K operands of step cc + 1 are read while the MFMAs of step cc run.
+  bf16x8 a[2][H::KT];
+#pragma unroll
+  for (int kt = 0; kt < H::KT; kt++)
+    a[0][kt] = *(const bf16x8*)(sk + (krow0 + 32 * kt) * T::RB + ((h ^ ksw) << 4));
 #pragma unroll
   for (int cc = 0; cc < T::DC; cc++) {
+    if (cc + 1 < T::DC) {
 #pragma unroll
-    for (int kt = 0; kt < H::KT; kt++) {
-      const bf16x8 a =
-          *(const bf16x8*)(sk + (krow0 + 32 * kt) * T::RB + (((2 * cc + h) ^ ksw) << 4));
-      s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, st.q[cc], cc == 0 ? st.negm : s[kt], 0, 0, 0);
+      for (int kt = 0; kt < H::KT; kt++)
+        a[(cc + 1) & 1][kt] =
+            *(const bf16x8*)(sk + (krow0 + 32 * kt) * T::RB + (((2 * (cc + 1) + h) ^ ksw) << 4));
     }
+    __builtin_amdgcn_sched_barrier(0);      // keep the reads ahead of this step's MFMAs
+#pragma unroll
+    for (int kt = 0; kt < H::KT; kt++)
+      s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cc & 1][kt], st.q[cc], cc == 0 ? st.negm : s[kt], 0, 0, 0);
   }
 }
 
@@ -920,11 +929,13 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
   // it issues ahead of the other wave on its SIMD, whose Q K^T MFMAs fill the gaps (measured:
   // 3 % faster sparse, 2-4 % dense).
   __builtin_amdgcn_s_setprio(1);
-  float mx = -__builtin_inff();
+  // Row max as four independent chains, then combined (a short dependent chain).
+  float m4[4] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
 #pragma unroll
   for (int kt = 0; kt < H::KT; kt++)
 #pragma unroll
-    for (int i = 0; i < 16; i++) mx = fmaxf(mx, s[kt][i]);
+    for (int i = 0; i < 16; i++) m4[i & 3] = fmaxf(m4[i & 3], s[kt][i]);
+  const float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
   const float base = -st.negm[0];
   const float ms = pair_max(mx) + base;
   const bool need = ms - st.m > 8.0f;     // false for -inf - -inf (NaN)
@@ -948,6 +959,20 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
   for (int j = 0; j < H::KC; j++) {
+    // The V^T operands of this chunk are read ahead of its exponentials, which hide the LDS
+    // latency.
+    bf16x8 va[T::DT];
+#pragma unroll
+    for (int dt = 0; dt < T::DT; dt++) {
+      const int dd = dt * 32 + 16 * (g & 1) + 4 * (j16 & 3);
+      const int lchunk = dd >> 3, inoff = (dd & 7) * 2;
+      const uint8_t* a0 = sv + (vkey + 16 * j) * T::RB + ((lchunk ^ vsw0) << 4) + inoff;
+      const uint8_t* a1 = sv + (vkey + 16 * j + 4) * T::RB + ((lchunk ^ vsw1) << 4) + inoff;
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a0);
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a1);
+      va[dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+    __builtin_amdgcn_sched_barrier(0);      // keep the reads ahead of the exponentials
     f32x8 e;
 #pragma unroll
     for (int x = 0; x < 8; x++) e[x] = __builtin_amdgcn_exp2f(s[j >> 1][8 * (j & 1) + x]);
@@ -959,16 +984,8 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
     st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 4, 5), ones, st.l, false);
     st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(p, p, 6, 7), ones, st.l, false);
 #pragma unroll
-    for (int dt = 0; dt < T::DT; dt++) {
-      const int dd = dt * 32 + 16 * (g & 1) + 4 * (j16 & 3);
-      const int lchunk = dd >> 3, inoff = (dd & 7) * 2;
-      const uint8_t* a0 = sv + (vkey + 16 * j) * T::RB + ((lchunk ^ vsw0) << 4) + inoff;
-      const uint8_t* a1 = sv + (vkey + 16 * j + 4) * T::RB + ((lchunk ^ vsw1) << 4) + inoff;
-      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a0);
-      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PSA_LDS s16x4*)a1);
-      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p, st.o[dt], 0, 0, 0);
-    }
+    for (int dt = 0; dt < T::DT; dt++)
+      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[dt], p, st.o[dt], 0, 0, 0);
   }
   __builtin_amdgcn_s_setprio(0);
 }
