@@ -8,23 +8,25 @@
 //   psa_sparse_kernel                          persistent block-sparse attention (Algorithm 2)
 //   psa_dense_kernel                           the same tile engine with every block kept
 //
-// Tile engine (one workgroup of 4 wave64s per query block of BLK rows, head dim D):
-//   * wave w = (qi, ki) = (w & 1, w >> 1) owns queries [qi*BLK/2, +BLK/2) of the query block and
-//     keys [ki*BLK/2, +BLK/2) of every key/value block.  Each wave runs its own online softmax
-//     over its key half; the two halves are merged once per work item.  This keeps the LDS
-//     read volume at one K and one V byte per 64 queries, inside the ~128 B/clk/CU LDS budget
-//     at full MFMA rate.
+// Tile engine (one workgroup of BLK/32 wave64s per query block of BLK rows, head dim D; two
+// workgroups per CU, so two waves share each SIMD):
+//   * every wave owns 32 query rows of the query block and all BLK keys of each key/value
+//     block; lane l holds row l & 31, lanes l and l ^ 32 split its keys.  A block is processed
+//     in two halves of BLK/2 keys, each with its own online-softmax update.
 //   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: K rows come from LDS (A operand), Q^T stays in
 //     registers (B operand).  K rows are read in a permuted order so that each lane's fp32
 //     accumulators hold 8 consecutive keys of every 16-key chunk, which is exactly the B operand
 //     layout of the next product: P^T needs no data movement.
 //   * O^T += V^T P^T: V stays row-major in LDS and the A operand is assembled with the gfx950 LDS
 //     transpose read (ds_read_b64_tr_b16).
-//   * K and V blocks are double-buffered in LDS and filled by direct global->LDS 16-byte loads
-//     (global_load_lds_dwordx4) issued one block ahead; 16-byte chunks are XOR-swizzled per row
-//     so both the K reads and the transposed V reads are bank-conflict free.
-//   * Softmax runs in the exp2 domain with scale*log2(e) folded into one FMA; the running max
-//     is raised lazily (only when a new max exceeds it by more than 2^8), which is exact.
+//   * One K and one V buffer per workgroup, filled by direct global->LDS 16-byte loads
+//     (global_load_lds_dwordx4) by halves: each half of the next block is issued as soon as the
+//     last reader of that half of the current block has passed a barrier.  16-byte chunks are
+//     XOR-swizzled per row so both the K reads and the transposed V reads are bank-conflict free.
+//   * Softmax in the exp2 domain: Q is multiplied by scale*log2(e) once, and the S^T
+//     accumulators start at -m, so the MFMAs deliver the exponent directly; the running max is
+//     raised lazily (only when a new max exceeds it by more than 8, i.e. P <= 2^8), which is
+//     exact.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
