@@ -1003,7 +1003,7 @@ __device__ __forceinline__ void softmax_pv_half(WaveState<D, BLK>& st,
 template <int D, int BLK, bool PAD>
 __device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<D, BLK>& plan,
                                            const __bf16* kh, const __bf16* vh, int kb, int kb_next,
-                                           int n, const uint8_t* sk, const uint8_t* sv,
+                                           bool more, int n, const uint8_t* sk, const uint8_t* sv,
                                            const uint64_t* masks, int lane) {
   uint64_t lo = ~0ull, hi = ~0ull;
   bool tail;
@@ -1017,7 +1017,6 @@ __device__ __forceinline__ void block_step(WaveState<D, BLK>& st, const DmaPlan<
   }
   using H = Half<D, BLK>;
   constexpr int HW = DmaPlan<D, BLK>::HW;
-  const bool more = kb_next >= 0;
   f32x16 s[H::KT];
   qk_half<D, BLK>(st, s, sk, 0, lane);
   wait_dma<HW>();                                       // V_lo(i), K_hi(i); V_hi(i) may fly
@@ -1081,20 +1080,41 @@ __device__ __forceinline__ void process_item(const DmaPlan<D, BLK>& plan,
 
   // Only the last block of a sequence can reach past its end, and it is always the last of an
   // ascending list.
-  auto kv = [&](int i) { return SPARSE ? (int)list[i] : i; };
-  if (nkv > 0) {
-    constexpr int HW = DmaPlan<D, BLK>::HW;
-    issue_half<D, BLK>(plan, kh, plan.lds_k, 0, kv(0), n);
-    issue_half<D, BLK>(plan, vh, plan.lds_v, 0, kv(0), n);
-    issue_half<D, BLK>(plan, kh, plan.lds_k, 1, kv(0), n);
-    issue_half<D, BLK>(plan, vh, plan.lds_v, 1, kv(0), n);
-    wait_dma<3 * HW>();                                 // K_lo(0)
-    __syncthreads();
-  }
-  for (int it = 0; it < nkv; it++) {
-    const int kb = kv(it);
-    const int kb_next = it + 1 < nkv ? kv(it + 1) : -1;
-    block_step<D, BLK, PAD>(st, plan, kh, vh, kb, kb_next, n, sk, sv, masks, lane);
+  constexpr int HW = DmaPlan<D, BLK>::HW;
+  if constexpr (SPARSE) {
+    // Block indices are read from the list two steps ahead and kept in vector registers until
+    // the step that issues their loads (issue_half takes the wave-uniform value), so no list
+    // read waits on the path into the next Q K^T.
+    int kb_v = 0, kb1_v = -1;
+    if (nkv > 0) {
+      kb_v = list[0];
+      kb1_v = nkv > 1 ? (int)list[1] : -1;
+      issue_half<D, BLK>(plan, kh, plan.lds_k, 0, kb_v, n);
+      issue_half<D, BLK>(plan, vh, plan.lds_v, 0, kb_v, n);
+      issue_half<D, BLK>(plan, kh, plan.lds_k, 1, kb_v, n);
+      issue_half<D, BLK>(plan, vh, plan.lds_v, 1, kb_v, n);
+      wait_dma<3 * HW>();                               // K_lo(0)
+      __syncthreads();
+    }
+    for (int it = 0; it < nkv; it++) {
+      const int kb2_v = it + 2 < nkv ? (int)list[it + 2] : -1;
+      block_step<D, BLK, PAD>(st, plan, kh, vh, __builtin_amdgcn_readfirstlane(kb_v), kb1_v,
+                              it + 1 < nkv, n, sk, sv, masks, lane);
+      kb_v = kb1_v;
+      kb1_v = kb2_v;
+    }
+  } else {
+    if (nkv > 0) {
+      issue_half<D, BLK>(plan, kh, plan.lds_k, 0, 0, n);
+      issue_half<D, BLK>(plan, vh, plan.lds_v, 0, 0, n);
+      issue_half<D, BLK>(plan, kh, plan.lds_k, 1, 0, n);
+      issue_half<D, BLK>(plan, vh, plan.lds_v, 1, 0, n);
+      wait_dma<3 * HW>();                               // K_lo(0)
+      __syncthreads();
+    }
+    for (int it = 0; it < nkv; it++)
+      block_step<D, BLK, PAD>(st, plan, kh, vh, it, it + 1 < nkv ? it + 1 : -1, it + 1 < nkv, n, sk,
+                              sv, masks, lane);
   }
 
   // Epilogue: O = O^T / l, rows past the end are not stored.
