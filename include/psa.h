@@ -24,6 +24,9 @@
  *  - Tensors are bf16, contiguous, layout [batch][n_heads][N][head_dim] (row-major).
  *  - Tensor pointers are device pointers owned by the caller; nothing is retained after the
  *    call.  `params` is a host array of n_heads entries, read before the call returns.
+ *  - Alignment: bf16 tensors 16 bytes (the kernels move 16-byte vectors), float and int32
+ *    arrays 4 bytes, int64 arrays 8 bytes; a misaligned pointer is rejected with
+ *    PSA_ERR_INVALID.
  *  - Every call only enqueues work on `stream` (0 = the null stream of the current device) and
  *    returns; results are ready after the caller synchronises that stream.  The current device
  *    must be the stream's device.
@@ -77,7 +80,8 @@ typedef struct {
 
 typedef enum {
   PSA_OK = 0,
-  PSA_ERR_INVALID = 1,     /* null pointer, width/stride < 1, |offset| too large, bad sizes */
+  PSA_ERR_INVALID = 1,     /* null or misaligned pointer, width/stride < 1, |offset| too large,
+                              bad sizes */
   PSA_ERR_UNSUPPORTED = 2, /* head_dim or block outside {64, 128}, too many blocks or heads */
   PSA_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than psa_workspace_size() */
   PSA_ERR_HIP = 4          /* a HIP runtime call failed; see psa_last_error() */

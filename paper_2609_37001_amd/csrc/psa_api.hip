@@ -92,6 +92,28 @@ psa_status_t geometry_3d(psa_grid_t grid, psa_block3d_t pb, int32_t tile, psa::G
   return PSA_OK;
 }
 
+// Alignment of a device pointer (NULL passes: optional outputs are checked for presence
+// separately).
+bool aligned(const void* p, uintptr_t bytes) { return ((uintptr_t)p & (bytes - 1)) == 0; }
+
+// The tensors of an attention call: q, k, v and o present and 16-byte aligned (the kernels load
+// and store 16-byte vectors), lse (optional) 4-byte aligned.
+psa_status_t check_tensors(const void* q, const void* k, const void* v, const void* o,
+                           const float* lse) {
+  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16))
+    return fail(PSA_ERR_INVALID, "q, k, v and o must be 16-byte aligned (%p %p %p %p)", q, k, v, o);
+  if (!aligned(lse, 4)) return fail(PSA_ERR_INVALID, "lse must be 4-byte aligned (%p)", (const void*)lse);
+  return PSA_OK;
+}
+
+// Optional count outputs of the map and plan calls.
+psa_status_t check_counts_out(const int32_t* per_row, const int64_t* per_head) {
+  if (!aligned(per_row, 4)) return fail(PSA_ERR_INVALID, "kept_per_row must be 4-byte aligned");
+  if (!aligned(per_head, 8)) return fail(PSA_ERR_INVALID, "kept_per_head must be 8-byte aligned");
+  return PSA_OK;
+}
+
 psa_status_t check_params(const psa_stripe_t* params, int32_t n_heads) {
   if (!params) return fail(PSA_ERR_INVALID, "params is NULL");
   if (n_heads < 1) return fail(PSA_ERR_INVALID, "n_heads must be >= 1 (got %d)", n_heads);
@@ -195,6 +217,8 @@ psa_status_t enqueue_plan(int32_t batch, int32_t n_heads, const psa::Geometry& g
 
 psa_status_t check_layout_args(const void* a, const void* b, int32_t n_bh, int32_t head_dim) {
   if (!a || !b) return fail(PSA_ERR_INVALID, "tensors must be non-NULL");
+  if (!aligned(a, 16) || !aligned(b, 16))
+    return fail(PSA_ERR_INVALID, "tensors must be 16-byte aligned (%p %p)", a, b);
   if (n_bh < 1) return fail(PSA_ERR_INVALID, "batch_heads must be >= 1 (got %d)", n_bh);
   if (n_bh > 65535) return fail(PSA_ERR_UNSUPPORTED, "batch_heads must be <= 65535 (got %d)", n_bh);
   if (head_dim != 64 && head_dim != 128)
@@ -262,6 +286,8 @@ psa_status_t psa_build_blockmap_3d(const psa_stripe_t* params, int32_t n_heads, 
   if (s != PSA_OK) return s;
   s = check_params(params, n_heads);
   if (s != PSA_OK) return s;
+  s = check_counts_out(kept_per_row, kept_per_head);
+  if (s != PSA_OK) return s;
   const int64_t groups = (int64_t)g.tp * g.hp * g.wp + (grid.n_text > 0 ? 1 : 0);
   if (groups * groups >= ((int64_t)1 << 40) || groups >= ((int64_t)1 << 31))
     return fail(PSA_ERR_UNSUPPORTED, "PSABlock map of %lld groups is too large", (long long)groups);
@@ -293,6 +319,8 @@ psa_status_t psa_attention_plan_3d(int32_t batch, int32_t n_heads, psa_grid_t gr
   if (s != PSA_OK) return s;
   s = check_params(params, n_heads);
   if (s != PSA_OK) return s;
+  s = check_counts_out(kept_per_tile, nullptr);
+  if (s != PSA_OK) return s;
   return enqueue_plan(batch, n_heads, g, params, workspace, wl, kept_per_tile, stream,
                       "psa_attention_plan_3d launch");
 }
@@ -302,8 +330,9 @@ psa_status_t psa_attention_run_3d(const void* q, const void* k, const void* v, v
                                   psa_grid_t grid, psa_block3d_t pb, int32_t tile,
                                   float softmax_scale, void* workspace, size_t workspace_bytes,
                                   float* lse, hipStream_t stream) {
-  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
-  psa_status_t s = check_attention_shape(batch, n_heads, head_dim, tile);
+  psa_status_t s = check_tensors(q, k, v, o, lse);
+  if (s != PSA_OK) return s;
+  s = check_attention_shape(batch, n_heads, head_dim, tile);
   if (s != PSA_OK) return s;
   psa::Geometry g;
   psa::WorkspaceLayout wl;
@@ -325,6 +354,8 @@ psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa
                 grid.height, grid.width, grid.n_text, block);
   psa_status_t s = check_params(params, n_heads);
   if (s != PSA_OK) return s;
+  s = check_counts_out(kept_per_row, kept_per_head);
+  if (s != PSA_OK) return s;
   if ((int64_t)g.nb * g.nb >= ((int64_t)1 << 40))
     return fail(PSA_ERR_UNSUPPORTED, "block map of %d x %d blocks is too large", g.nb, g.nb);
   for (int32_t h0 = 0; h0 < n_heads; h0 += psa::kHeadsPerChunk) {
@@ -345,6 +376,8 @@ psa_status_t psa_attention_plan(int32_t batch, int32_t n_heads, psa_grid_t grid,
   if (s != PSA_OK) return s;
   s = check_params(params, n_heads);
   if (s != PSA_OK) return s;
+  s = check_counts_out(kept_per_row, nullptr);
+  if (s != PSA_OK) return s;
   return enqueue_plan(batch, n_heads, g, params, workspace, wl, kept_per_row, stream,
                       "psa_attention_plan launch");
 }
@@ -353,8 +386,9 @@ psa_status_t psa_attention_run(const void* q, const void* k, const void* v, void
                                int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
                                int32_t block, float softmax_scale, void* workspace,
                                size_t workspace_bytes, float* lse, hipStream_t stream) {
-  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
-  psa_status_t s = check_attention_shape(batch, n_heads, head_dim, block);
+  psa_status_t s = check_tensors(q, k, v, o, lse);
+  if (s != PSA_OK) return s;
+  s = check_attention_shape(batch, n_heads, head_dim, block);
   if (s != PSA_OK) return s;
   psa::Geometry g;
   psa::WorkspaceLayout wl;
@@ -372,8 +406,9 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
                                int32_t block, const psa_stripe_t* params, float softmax_scale,
                                void* workspace, size_t workspace_bytes, float* lse,
                                int32_t* kept_per_row, hipStream_t stream) {
-  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
-  psa_status_t s = check_attention_shape(batch, n_heads, head_dim, block);
+  psa_status_t s = check_tensors(q, k, v, o, lse);
+  if (s != PSA_OK) return s;
+  s = check_attention_shape(batch, n_heads, head_dim, block);
   if (s != PSA_OK) return s;
   s = psa_attention_plan(batch, n_heads, grid, block, params, workspace, workspace_bytes,
                          kept_per_row, stream);
@@ -385,8 +420,9 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
 psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o, int32_t batch,
                            int32_t n_heads, int32_t head_dim, int32_t n_tokens, int32_t block,
                            float softmax_scale, float* lse, hipStream_t stream) {
-  if (!q || !k || !v || !o) return fail(PSA_ERR_INVALID, "q, k, v and o must be non-NULL");
-  psa_status_t s = check_attention_shape(batch, n_heads, head_dim, block);
+  psa_status_t s = check_tensors(q, k, v, o, lse);
+  if (s != PSA_OK) return s;
+  s = check_attention_shape(batch, n_heads, head_dim, block);
   if (s != PSA_OK) return s;
   if (n_tokens < 1 || (int64_t)n_tokens + 2 * block >= ((int64_t)1 << 31))
     return fail(PSA_ERR_INVALID, "n_tokens must be in [1, 2^31 - 2*block) (got %d)", n_tokens);
@@ -413,11 +449,14 @@ psa_status_t psa_l2_distance(const void* o, const void* ref, int32_t batch_heads
     return fail(PSA_ERR_UNSUPPORTED, "batch_heads must be <= 65535 (got %d)", batch_heads);
   if (head_dim < 8 || head_dim % 8 != 0)
     return fail(PSA_ERR_UNSUPPORTED, "head_dim must be a positive multiple of 8 (got %d)", head_dim);
-  if (((uintptr_t)o & 15) != 0 || ((uintptr_t)ref & 15) != 0)
+  if (!aligned(o, 16) || !aligned(ref, 16))
     return fail(PSA_ERR_INVALID, "o and ref must be 16-byte aligned");
+  if (!aligned(sq_err, 8) || !aligned(sq_ref, 8))
+    return fail(PSA_ERR_INVALID, "sq_err and sq_ref must be 8-byte aligned");
   if (!workspace || workspace_bytes < psa_l2_workspace_size(batch_heads))
     return fail(PSA_ERR_WORKSPACE, "workspace of %zu bytes; %zu bytes required", workspace_bytes,
                 psa_l2_workspace_size(batch_heads));
+  if (!aligned(workspace, 8)) return fail(PSA_ERR_WORKSPACE, "workspace must be 8-byte aligned");
   hipError_t e = psa::launch_l2(o, ref, batch_heads, (int64_t)n_tokens * head_dim, (double*)workspace,
                                 sq_err, sq_ref, stream);
   return e == hipSuccess ? PSA_OK : hip_fail(e, "psa_l2_distance launch");

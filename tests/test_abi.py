@@ -47,8 +47,9 @@ def _attn(q=1, k=1, v=1, o=1, batch=1, heads=1, d=128, grid=(2, 8, 8, 0), block=
     L = _lib.lib()
     params = [(1, 0, INF, 1, 0, INF)] * heads if params is None else params
     vp = lambda x: ctypes.c_void_p(x) if x else None
-    return L.psa_attention_fwd(vp(q), vp(k), vp(v), vp(o), batch, heads, d, _lib.grid_of(*grid), block,
-                               _lib.stripes(params), scale, vp(ws * 256), wsb, None, None, None)
+    return L.psa_attention_fwd(vp(q * 256), vp(k * 256), vp(v * 256), vp(o * 256), batch, heads, d,
+                               _lib.grid_of(*grid), block, _lib.stripes(params), scale, vp(ws * 256), wsb,
+                               None, None, None)
 
 
 def test_attention_validation_codes():
@@ -111,8 +112,8 @@ def _plan(batch=1, heads=1, grid=(2, 8, 8, 0), block=128, params=None, ws=1, wsb
 def _run(q=1, o=1, batch=1, heads=1, d=128, grid=(2, 8, 8, 0), block=128, ws=1, wsb=1 << 20):
     L = _lib.lib()
     vp = lambda x: ctypes.c_void_p(x) if x else None
-    return L.psa_attention_run(vp(q), vp(256), vp(256), vp(o), batch, heads, d, _lib.grid_of(*grid),
-                               block, 0.1, vp(ws * 256), wsb, None, None)
+    return L.psa_attention_run(vp(q * 256), vp(256), vp(256), vp(o * 256), batch, heads, d,
+                               _lib.grid_of(*grid), block, 0.1, vp(ws * 256), wsb, None, None)
 
 
 def test_plan_validation_codes():
@@ -196,3 +197,47 @@ def test_plan_and_run_3d_validation_codes():
     assert run(d=80) == _lib.PSA_ERR_UNSUPPORTED
     assert run(tile=96) == _lib.PSA_ERR_UNSUPPORTED
     assert run(pb=(1, 3, 5)) == _lib.PSA_ERR_UNSUPPORTED
+
+
+def test_misaligned_pointers_are_rejected():
+    """The kernels move 16-byte vectors: a misaligned tensor is an argument error, checked before
+    anything is enqueued (no GPU is needed to see it)."""
+    L = _lib.lib()
+    vp = lambda x: ctypes.c_void_p(x) if x else None
+    params = _lib.stripes([(1, 0, INF, 1, 0, INF)])
+    g = _lib.grid_of(2, 8, 8, 0)
+    fwd = lambda q=256, k=256, v=256, o=256, lse=None, kept=None: L.psa_attention_fwd(
+        vp(q), vp(k), vp(v), vp(o), 1, 1, 128, g, 128, params, 0.1, vp(256), 1 << 20, vp(lse), vp(kept), None)
+    assert fwd(q=256 + 8) == _lib.PSA_ERR_INVALID
+    assert fwd(k=256 + 2) == _lib.PSA_ERR_INVALID
+    assert fwd(v=256 + 4) == _lib.PSA_ERR_INVALID
+    assert fwd(o=256 + 12) == _lib.PSA_ERR_INVALID
+    assert fwd(lse=256 + 2) == _lib.PSA_ERR_INVALID
+    assert b"aligned" in L.psa_last_error()
+    assert fwd(kept=256 + 1) == _lib.PSA_ERR_INVALID
+    run = lambda q=256, o=256, lse=None: L.psa_attention_run(vp(q), vp(256), vp(256), vp(o), 1, 1, 128, g, 128,
+                                                             0.1, vp(256), 1 << 20, vp(lse), None)
+    assert run(q=264) == _lib.PSA_ERR_INVALID
+    assert run(o=258) == _lib.PSA_ERR_INVALID
+    assert run(lse=257) == _lib.PSA_ERR_INVALID
+    dense = lambda q=256, lse=None: L.psa_dense_fwd(vp(q), vp(256), vp(256), vp(256), 1, 1, 128, 256, 128,
+                                                    0.1, vp(lse), None)
+    assert dense(q=264) == _lib.PSA_ERR_INVALID
+    assert dense(lse=258) == _lib.PSA_ERR_INVALID
+    b3 = _b3(2, 4, 16)
+    g3 = _lib.grid_of(4, 10, 20, 0)
+    assert L.psa_attention_run_3d(vp(256), vp(256), vp(264), vp(256), 1, 1, 128, g3, b3, 128, 0.1, vp(256),
+                                  1 << 20, None, None) == _lib.PSA_ERR_INVALID
+    assert L.psa_to_blocks(vp(264), vp(256), 1, 128, g3, b3, None) == _lib.PSA_ERR_INVALID
+    assert L.psa_from_blocks(vp(256), vp(260), 1, 128, g3, b3, None) == _lib.PSA_ERR_INVALID
+    assert L.psa_build_blockmap(params, 1, g, 128, None, vp(258), None, None) == _lib.PSA_ERR_INVALID
+    assert L.psa_build_blockmap(params, 1, g, 128, None, None, vp(260), None) == _lib.PSA_ERR_INVALID
+    assert L.psa_build_blockmap_3d(params, 1, g3, b3, None, None, vp(260), None) == _lib.PSA_ERR_INVALID
+    assert L.psa_attention_plan(1, 1, g, 128, params, vp(256), 1 << 20, vp(258), None) == _lib.PSA_ERR_INVALID
+    assert L.psa_attention_plan_3d(1, 1, g3, b3, 128, params, vp(256), 1 << 20, vp(258),
+                                   None) == _lib.PSA_ERR_INVALID
+    l2 = lambda o=256, err=512, ws=1024: L.psa_l2_distance(vp(o), vp(256), 1, 64, 128, vp(err), None, vp(ws),
+                                                           4096, None)
+    assert l2(o=264) == _lib.PSA_ERR_INVALID
+    assert l2(err=516) == _lib.PSA_ERR_INVALID
+    assert l2(ws=1028) == _lib.PSA_ERR_WORKSPACE

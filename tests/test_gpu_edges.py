@@ -118,3 +118,26 @@ def test_binding_rejects_bad_tensors():
     with pytest.raises(psa.PsaError):
         psa.attention_fwd(x[:, :, :, :96].contiguous(), x[:, :, :, :96].contiguous(),
                           x[:, :, :, :96].contiguous(), (1, 8, 16), 128, [(1, 0, INF, 1, 0, INF)])
+
+
+def test_binding_rejects_misaligned_tensors():
+    """A contiguous view that starts one element into its storage is not 16-byte aligned: the
+    library rejects it (PSA_ERR_INVALID) before any kernel runs, and the binding raises."""
+    torch = gu.torch()
+    x = torch.zeros((1, 1, 128, 128), dtype=torch.bfloat16, device="cuda:0")
+    flat = torch.zeros(128 * 128 + 8, dtype=torch.bfloat16, device="cuda:0")
+    y = flat[1:1 + 128 * 128].view(1, 1, 128, 128)
+    assert y.is_contiguous() and y.data_ptr() % 16 != 0
+    stripes = [(1, 0, INF, 1, 0, INF)]
+    for args in ((y, x, x), (x, y, x), (x, x, y)):
+        with pytest.raises(psa.PsaError) as e:
+            psa.attention_fwd(*args, (1, 8, 16), 128, stripes)
+        assert e.value.status == _lib.PSA_ERR_INVALID
+    with pytest.raises(psa.PsaError):
+        psa.dense_fwd(y, x, x, 128, 0.1)
+    with pytest.raises(psa.PsaError):
+        psa.attention_fwd(x, x, x, (1, 8, 16), 128, stripes, out=y)
+    torch.cuda.synchronize()
+    o = psa.attention_fwd(x, x, x, (1, 8, 16), 128, stripes)     # the library still works
+    torch.cuda.synchronize()
+    assert torch.isfinite(o.float()).all()
