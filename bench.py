@@ -35,8 +35,10 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA peak (published)
 HBM_PEAK = 8.0e12             # MI355X HBM3E bandwidth, bytes/s (published)
-KERNEL = "psa_sparse_kernel<128, 128, false>"
-COUNTERS_MD = os.path.join(ROOT, "profiles", "psa_sparse_kernel_wan14b_counters.md")
+KERNEL = "psa_pair_kernel<128, 128, true, false>"       # the sparse attention at block 128
+KERNEL_3D = "psa_pair_kernel<128, 128, true, true>"     # ... with the 3D-padding masks
+ATTN_PREFIXES = ("psa_sparse_kernel", "psa_dense_kernel", "psa_pair_kernel")  # attention kernels
+COUNTERS_MD = os.path.join(ROOT, "profiles", "psa_pair_kernel_wan14b_counters.md")
 SOURCES = ("paper_2609_37001_amd/csrc/psa_kernels.hip", "paper_2609_37001_amd/csrc/psa_launch.h",
            "paper_2609_37001_amd/csrc/psa_api.hip", "paper_2609_37001_amd/build.py", "include/psa.h")
 WORKLOAD_TEXT = {
@@ -154,7 +156,7 @@ def summarise_counters(fetch_dir, write_dir, copy_mb):
     copy_bytes = copy_mb * 1048576.0
     f_copy, w_copy = max(pick(fetch, "copyBuffer")), max(pick(write, "copyBuffer"))
     f_scale, w_scale = copy_bytes / (f_copy * 1024.0), copy_bytes / (w_copy * 1024.0)
-    f_k, w_k = pick(fetch, "psa_sparse_kernel"), pick(write, "psa_sparse_kernel")
+    f_k, w_k = pick(fetch, KERNEL), pick(write, KERNEL)
     f_mean, w_mean = sum(f_k) / len(f_k), sum(w_k) / len(w_k)
     traffic = f_mean * 1024.0 * f_scale + w_mean * 1024.0 * w_scale
     lines = [
@@ -187,7 +189,7 @@ def summarise_counters(fetch_dir, write_dir, copy_mb):
         "",
         "Algorithmic bytes per launch: Q, K, V read once and O written once, "
         "4 x 40 x 75600 x 128 x 2 B = 3.097e9 B.  Traffic above that is K/V tiles that missed "
-        "the L2 (each kept tile is streamed once per query block).",
+        "the L2 (each kept tile is streamed once per pair of query blocks).",
     ]
     return "\n".join(lines) + "\n"
 
@@ -216,7 +218,7 @@ def utilisation_rows(sq_dir, tcc_dir, trace_dir, label):
             with open(path) as f:
                 for r in csv.DictReader(f):
                     name = r["Kernel_Name"].split("(")[0].replace("void ", "").replace("psa::", "")
-                    if name.startswith(("psa_sparse", "psa_dense")):
+                    if name.startswith(ATTN_PREFIXES):
                         out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
         return {k: {c: sum(v) / len(v) for c, v in d.items()} for k, d in out.items()}
     sq, tcc = per_kernel(sq_dir), per_kernel(tcc_dir)
@@ -260,7 +262,7 @@ def hbm_rows(fetch_dir, write_dir, trace_dir, cfg, copy_mb):
     rows = []
     for full, vals in sorted(fetch.items()):
         k = full.split("(")[0].replace("void ", "").replace("psa::", "")
-        if not k.startswith(("psa_sparse", "psa_dense")):
+        if not k.startswith(ATTN_PREFIXES):
             continue
         wv = [v for kk, v in write.items() if kk.split("(")[0].replace("void ", "").replace("psa::", "") == k][0]
         rd = sum(vals) / len(vals) * 1024.0 * f_scale
@@ -284,7 +286,7 @@ def wait_rows(run_dir, label):
         with open(path) as f:
             for r in csv.DictReader(f):
                 name = r["Kernel_Name"].split("(")[0].replace("void ", "").replace("psa::", "")
-                if name.startswith(("psa_sparse", "psa_dense")):
+                if name.startswith(ATTN_PREFIXES):
                     out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     rows = []
     for k in sorted(out):
@@ -466,7 +468,7 @@ def bench_3d(args, cfg, params, torch, psa):
                        "speedup_vs_dense_with_layout": round(dms / (ms + t_to["mean"] + t_from["mean"]), 3)})
         log("dense (original order, unpadded): %.3f ms, speedup %.3f (%.3f with the layout conversions)"
             % (dms, dms / ms, dms / (ms + t_to["mean"] + t_from["mean"])))
-    result["roofline"] = {"kernel": "psa_sparse_kernel<128, 128, true>", "bound": "mfma",
+    result["roofline"] = {"kernel": KERNEL_3D, "bound": "mfma",
                           "achieved": round(k_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                           "frac": round(k_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None}
     print(json.dumps(result), flush=True)

@@ -92,8 +92,9 @@ int32_t psa_num_blocks(psa_grid_t grid, int32_t block);
 
 /* Bytes of device workspace psa_attention_plan / psa_attention_fwd need for these sizes
  * (0 if invalid).  The workspace holds a plan: the per-head parameters, the block coordinates,
- * the kept-block count of every (batch, head, query block) work item, the load-balanced work
- * order, the queue counters and a header naming the sizes the plan was made for. */
+ * the work of every work item, the load-balanced work order, the queue counters and a header
+ * naming the sizes the plan was made for; at block 128 also a signature of each query block's
+ * kept set and the pairs of query blocks that form the work items. */
 size_t psa_workspace_size(int32_t batch, int32_t n_heads, psa_grid_t grid, int32_t block);
 
 /* Block map of Algorithm 1 at block granularity (Sec. 3.2), computed on the device by the same
@@ -109,7 +110,10 @@ psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa
 
 /* Plan of psa_attention_run (the work list of Algorithm 2 without the attention itself): copies
  * the stripe parameters of each head to the workspace, counts the kept key blocks of every
- * (batch, head, query block) work item with the Algorithm 1 decoder and orders the items: those
+ * work item with the Algorithm 1 decoder and orders the items.  A work item is one (batch, head,
+ * query block) at block 64; at block 128 it is a pair of query blocks of one (batch, head) that
+ * share one K/V stream, the pairs formed from query blocks with equal kept sets first (the rest
+ * in index order) and weighed by the union of the two sets.  Order: items
  * of more than three times the mean work (rows that keep every key block, such as text rows)
  * first, longest first, then the heads longest first, each split into equal-work ranges, one
  * work queue per XCD.  The plan
@@ -125,8 +129,8 @@ psa_status_t psa_attention_plan(int32_t batch, int32_t n_heads, psa_grid_t grid,
                                 hipStream_t stream);
 
 /* Sparse attention over a planned workspace (Algorithm 2): one persistent kernel whose
- * workgroups pop query blocks from the plan's queues, decode each one's kept key blocks
- * (Algorithm 1) and run the tile engine over them.  Arguments as in psa_attention_fwd.  The
+ * workgroups pop work items from the plan's queues, decode the kept key blocks of each query
+ * block (Algorithm 1) and run the tile engine over them.  Arguments as in psa_attention_fwd.  The
  * workspace must hold a plan made for the same batch, n_heads, grid and block; the kernel checks
  * the plan's header first and, on a mismatch or an unfinished plan, writes nothing (o and lse keep
  * their contents; no error can be returned for a condition found on the device).  The run

@@ -349,7 +349,9 @@ WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb, boo
   wl.counts = up(wl.coords + sizeof(int2) * (size_t)nb);
   wl.order = up(wl.counts + sizeof(int32_t) * items);
   wl.queues = up(wl.order + sizeof(int32_t) * items);
-  wl.masks = up(wl.queues + sizeof(int32_t) * kQueueWords);
+  wl.sigs = up(wl.queues + sizeof(int32_t) * kQueueWords);
+  wl.pairs = up(wl.sigs + sizeof(uint64_t) * (size_t)n_heads * nb);
+  wl.masks = up(wl.pairs + sizeof(int2) * (size_t)n_heads * pairs_per_head(nb));
   wl.total = masks ? up(wl.masks + 2 * sizeof(uint64_t) * (size_t)nb) : wl.masks;
   return wl;
 }
@@ -402,11 +404,23 @@ hipError_t launch_setup(const ParamChunk& pc, int32_t head0, const Geometry& g, 
   return hipGetLastError();
 }
 
-// One wave per work item (batch, head, query block): number of kept key blocks.
+// A 64-bit mix of a block index (the splitmix64 finalizer); the XOR of the mixes of a kept set
+// is a hash of the set that does not depend on the order of its members.
+__device__ __forceinline__ uint64_t mix64(uint64_t x) {
+  x += 0x9e3779b97f4a7c15ull;
+  x = (x ^ (x >> 30)) * 0xbf58476d1ce4e5b9ull;
+  x = (x ^ (x >> 27)) * 0x94d049bb133111ebull;
+  return x ^ (x >> 31);
+}
+
+// One wave per work item (batch, head, query block): number of kept key blocks (counts, or
+// nullptr), and for the items of the first batch element the per-row count (kept_per_row) and
+// the signature of the kept set (sigs), each if asked.
 __global__ __launch_bounds__(256) void psa_count_kernel(const psa_stripe_t* __restrict__ params,
                                                         const int2* __restrict__ coords,
                                                         int32_t* __restrict__ counts,
                                                         int32_t* __restrict__ kept_per_row,
+                                                        uint64_t* __restrict__ sigs,
                                                         int32_t n_items, int32_t n_heads,
                                                         int32_t nb) {
   const int32_t item = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -415,12 +429,163 @@ __global__ __launch_bounds__(256) void psa_count_kernel(const psa_stripe_t* __re
   const psa_stripe_t m = params[h];
   const int2 cq = coords[qb];
   int cnt = 0;
-  for (int32_t kb = lane; kb < nb; kb += 64) cnt += tile_keep(m, cq, coords[kb]) ? 1 : 0;
-  cnt = wave_sum(cnt);
-  if (lane == 0) {
-    counts[item] = cnt;
-    if (kept_per_row && bh < n_heads) kept_per_row[(int64_t)h * nb + qb] = cnt;
+  uint64_t sig = 0;
+  for (int32_t kb = lane; kb < nb; kb += 64) {
+    const bool keep = tile_keep(m, cq, coords[kb]);
+    cnt += keep ? 1 : 0;
+    sig ^= keep ? mix64((uint64_t)kb) : 0ull;
   }
+  cnt = wave_sum(cnt);
+  for (int off = 32; off > 0; off >>= 1) sig ^= __shfl_xor(sig, off);
+  if (lane == 0) {
+    if (counts) counts[item] = cnt;
+    if (bh < n_heads) {
+      if (kept_per_row) kept_per_row[(int64_t)h * nb + qb] = cnt;
+      if (sigs) sigs[(int64_t)h * nb + qb] = sig;
+    }
+  }
+}
+
+// Exclusive prefix sum (OP = +) or inclusive running maximum (OP = max) over v[0 .. n) in LDS by
+// a 1024-thread workgroup; n <= 8 * 1024.  Returns the total (sum) or the last value (max).
+template <bool MAX>
+__device__ int32_t block_scan(int32_t* v, int32_t n, int32_t* part) {
+  constexpr int E = 8;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int32_t loc[E];
+  int32_t acc = MAX ? -1 : 0;
+#pragma unroll
+  for (int e = 0; e < E; e++) {
+    const int32_t i = tid * E + e;
+    const int32_t x = i < n ? v[i] : (MAX ? -1 : 0);
+    loc[e] = acc;                                         // exclusive within the thread
+    acc = MAX ? max(acc, x) : acc + x;
+  }
+  int32_t incl = acc;                                     // inclusive over the wave
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t t = __shfl_up(incl, off);
+    if (lane >= off) incl = MAX ? max(incl, t) : incl + t;
+  }
+  if (lane == 63) part[wave] = incl;
+  __syncthreads();
+  int32_t before = MAX ? -1 : 0;                          // over the waves before this one
+  for (int w = 0; w < wave; w++) before = MAX ? max(before, part[w]) : before + part[w];
+  int32_t total = MAX ? -1 : 0;
+  for (int w = 0; w < 16; w++) total = MAX ? max(total, part[w]) : total + part[w];
+  const int32_t lane_excl = __shfl_up(incl, 1);
+  const int32_t prior = lane == 0 ? before : (MAX ? max(before, lane_excl) : before + lane_excl);
+#pragma unroll
+  for (int e = 0; e < E; e++) {
+    const int32_t i = tid * E + e;
+    if (i < n) {
+      if (MAX)
+        v[i] = max(prior, max(loc[e], v[i]));             // inclusive running maximum
+      else
+        v[i] = prior + loc[e];
+    }
+  }
+  __syncthreads();
+  return total;
+}
+
+// One workgroup per head: pairs of query blocks for the pair engine.  The rows are sorted by the
+// signature of their kept set (then by index); within a run of equal signatures consecutive
+// rows pair up; the rows left over pair up in index order.  pairs[h][p] = (first row, second
+// row or -1), in the order of the first rows.  Rows with equal kept sets share every key block,
+// so most pairs of the stripe patterns waste no work; the pairing only affects speed, the
+// run decodes each row's own kept set.
+constexpr int kPairSort = 8192;                 // a power of two >= PSA_MAX_BLOCKS
+__global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __restrict__ sigs,
+                                                           int2* __restrict__ pairs, int32_t nb) {
+  __shared__ uint64_t key[kPairSort];         // sorted (signature, row); later leftover rows
+  __shared__ int32_t run[kPairSort];          // start of each sorted position's run
+  __shared__ int16_t partner[kPairSort];      // by row: partner (first row), -1 single, -2 second
+  __shared__ int32_t part[16];
+  const int tid = threadIdx.x;
+  const uint64_t* sg = sigs + (size_t)blockIdx.x * nb;
+  int32_t n2 = 1;
+  while (n2 < nb) n2 <<= 1;
+  for (int32_t i = tid; i < n2; i += 1024) {
+    key[i] = i < nb ? ((sg[i] >> 13) << 13) | (uint64_t)i : ~0ull;
+    partner[i] = -3;
+  }
+  __syncthreads();
+  for (int32_t k = 2; k <= n2; k <<= 1)
+    for (int32_t j = k >> 1; j > 0; j >>= 1) {
+      for (int32_t i = tid; i < n2; i += 1024) {
+        const int32_t ixj = i ^ j;
+        if (ixj > i) {
+          const uint64_t a = key[i], b = key[ixj];
+          if ((a > b) == ((i & k) == 0)) {
+            key[i] = b;
+            key[ixj] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  auto row_of = [&](int32_t i) { return (int32_t)(key[i] & 8191u); };
+  auto same = [&](int32_t i, int32_t j) { return (key[i] >> 13) == (key[j] >> 13); };
+  for (int32_t i = tid; i < nb; i += 1024) run[i] = (i == 0 || !same(i, i - 1)) ? i : -1;
+  __syncthreads();
+  block_scan<true>(run, nb, part);
+  for (int32_t i = tid; i < nb; i += 1024) {
+    if (((i - run[i]) & 1) != 0) continue;
+    const int32_t r = row_of(i);
+    if (i + 1 < nb && run[i + 1] == run[i]) {
+      const int32_t r2 = row_of(i + 1);
+      partner[min(r, r2)] = (int16_t)max(r, r2);
+      partner[max(r, r2)] = -2;
+    } else {
+      partner[r] = -4;                                  // left over
+    }
+  }
+  __syncthreads();
+  // Leftover rows in index order: rank by a prefix sum over the rows, pair ranks 2k and 2k + 1.
+  for (int32_t i = tid; i < nb; i += 1024) run[i] = partner[i] == -4 ? 1 : 0;
+  __syncthreads();
+  const int32_t n_left = block_scan<false>(run, nb, part);
+  uint32_t* left = (uint32_t*)key;                        // rank -> row
+  for (int32_t i = tid; i < nb; i += 1024)
+    if (partner[i] == -4) left[run[i]] = (uint32_t)i;
+  __syncthreads();
+  for (int32_t i = tid; i < nb; i += 1024)
+    if (partner[i] == -4) {
+      const int32_t r = run[i];
+      partner[i] = (r & 1) ? -2 : (r + 1 < n_left ? (int16_t)left[r + 1] : -1);
+    }
+  __syncthreads();
+  // Pairs in the order of their first rows.
+  for (int32_t i = tid; i < nb; i += 1024) run[i] = partner[i] >= -1 ? 1 : 0;
+  __syncthreads();
+  block_scan<false>(run, nb, part);
+  int2* dst = pairs + (size_t)blockIdx.x * pairs_per_head(nb);
+  for (int32_t i = tid; i < nb; i += 1024)
+    if (partner[i] >= -1 && run[i] < pairs_per_head(nb)) dst[run[i]] = make_int2(i, partner[i]);
+}
+
+// One wave per pair item (batch, head, pair): number of key blocks kept by either row.
+__global__ __launch_bounds__(256) void psa_paircount_kernel(const psa_stripe_t* __restrict__ params,
+                                                            const int2* __restrict__ coords,
+                                                            const int2* __restrict__ pairs,
+                                                            int32_t* __restrict__ counts,
+                                                            int32_t n_items, int32_t n_heads,
+                                                            int32_t nb) {
+  const int32_t np = pairs_per_head(nb);
+  const int32_t item = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (item >= n_items) return;
+  const int32_t bh = item / np, p = item - bh * np, h = bh % n_heads;
+  const psa_stripe_t m = params[h];
+  const int2 pr = pairs[(int64_t)h * np + p];
+  const int2 ca = coords[pr.x];
+  const int2 cb = pr.y >= 0 ? coords[pr.y] : make_int2(kDeadTile, 0);
+  int cnt = 0;
+  for (int32_t kb = lane; kb < nb; kb += 64) {
+    const int2 ck = coords[kb];
+    cnt += (tile_keep(m, ca, ck) || tile_keep(m, cb, ck)) ? 1 : 0;
+  }
+  cnt = wave_sum(cnt);
+  if (lane == 0) counts[item] = cnt;
 }
 
 // Work estimate of an item, in tiles: kept key blocks plus a fixed cost for loading Q,
@@ -687,19 +852,41 @@ static PlanHeader plan_header(const Geometry& g, int32_t batch, int32_t n_heads)
   return h;
 }
 
+// Whether the attention of this geometry runs on the pair engine (work items are pairs of
+// query blocks) or on one query block per work item.
+static bool pair_engine(const Geometry& g) { return g.block == 128; }
+
 hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, void* workspace,
                            const WorkspaceLayout& wl, int32_t* kept_per_row, hipStream_t stream) {
   char* ws = (char*)workspace;
-  const int32_t n_items = batch * n_heads * g.nb;
-  hipLaunchKernelGGL(psa_count_kernel, dim3((n_items + 3) / 4), dim3(256), 0, stream,
-                     (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
-                     (int32_t*)(ws + wl.counts), kept_per_row, n_items, n_heads, g.nb);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(psa_schedule_kernel, dim3(1), dim3(1024), 0, stream,
-                     (const int32_t*)(ws + wl.counts), (int32_t*)(ws + wl.order),
-                     (int32_t*)(ws + wl.queues), (PlanHeader*)(ws + wl.header),
-                     plan_header(g, batch, n_heads), g.nb);
+  const psa_stripe_t* params = (const psa_stripe_t*)(ws + wl.params);
+  const int2* coords = (const int2*)(ws + wl.coords);
+  int32_t* counts = (int32_t*)(ws + wl.counts);
+  int32_t per_head = g.nb;
+  hipError_t e;
+  if (pair_engine(g)) {
+    // Row counts and kept-set signatures of one batch element, the pairs of each head, then the
+    // work of every pair item.
+    const int32_t n_rows = n_heads * g.nb;
+    hipLaunchKernelGGL(psa_count_kernel, dim3((n_rows + 3) / 4), dim3(256), 0, stream, params, coords,
+                       nullptr, kept_per_row, (uint64_t*)(ws + wl.sigs), n_rows, n_heads, g.nb);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(psa_pairing_kernel, dim3(n_heads), dim3(1024), 0, stream,
+                       (const uint64_t*)(ws + wl.sigs), (int2*)(ws + wl.pairs), g.nb);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    per_head = pairs_per_head(g.nb);
+    const int32_t n_items = batch * n_heads * per_head;
+    hipLaunchKernelGGL(psa_paircount_kernel, dim3((n_items + 3) / 4), dim3(256), 0, stream, params, coords,
+                       (const int2*)(ws + wl.pairs), counts, n_items, n_heads, g.nb);
+  } else {
+    const int32_t n_items = batch * n_heads * g.nb;
+    hipLaunchKernelGGL(psa_count_kernel, dim3((n_items + 3) / 4), dim3(256), 0, stream, params, coords,
+                       counts, kept_per_row, nullptr, n_items, n_heads, g.nb);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(psa_schedule_kernel, dim3(1), dim3(1024), 0, stream, (const int32_t*)counts,
+                     (int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues), (PlanHeader*)(ws + wl.header),
+                     plan_header(g, batch, n_heads), per_head);
   return hipGetLastError();
 }
 
@@ -1257,6 +1444,284 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
                               lse ? lse + (size_t)bh * n : nullptr, n, qb, nb, nullptr, c, sk, sv);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Pair engine (BLK = 128): one workgroup of eight waves per CU.  Waves 0-3 take the first query
+// block of a work item, waves 4-7 the second (each wave 32 rows, the per-wave tile engine
+// above).  The two rows share one stream of K/V blocks -- the union of their kept sets, each
+// entry marked with the rows that keep it -- double-buffered in LDS with one barrier per block
+// and every block's loads issued a whole block ahead; a row skips the blocks it does not keep.
+// The plan pairs rows with equal kept sets, so a K/V block is loaded once for two query blocks
+// and most entries are used by both rows.  Each row still visits its own kept blocks in
+// ascending order with the same arithmetic, so its output is that of the one-row engine.
+// ---------------------------------------------------------------------------------------------
+
+// Direct global->LDS loads of a whole K or V block by the eight waves of a workgroup: wave w
+// loads the 1 KB slots w S .. w S + S - 1, with the row/chunk mapping and swizzle of DmaPlan.
+template <int D, int BLK>
+struct DmaPlan8 {
+  using T = Tile<D, BLK>;
+  static constexpr int S = T::BYTES / (1024 * 8);      // slots per wave per tensor
+  static_assert(S >= 1 && T::BYTES % (1024 * 8) == 0, "tile shape");
+  uint32_t off[S];
+  int wave, lane;
+
+  __device__ __forceinline__ void init(int wave_, int lane_) {
+    wave = wave_;
+    lane = lane_;
+#pragma unroll
+    for (int i = 0; i < S; i++) off[i] = offset(i, BLK);
+  }
+
+  // Byte offset in the block of the 16 bytes this lane loads for slot i; rows at or past `rows`
+  // are clamped to row rows - 1 (their scores are masked).
+  __device__ __forceinline__ uint32_t offset(int i, int rows) const {
+    const int p = (wave * S + i) * 64 + lane;
+    const int row = p / T::CPR;
+    const int chunk = (p % T::CPR) ^ swz<T::CPR>(row);
+    return (uint32_t)(min(row, rows - 1) * T::RB + chunk * 16);
+  }
+};
+
+// Loads block kb of one tensor.  Waves 0-3 hold rows 0 .. BLK/2-1 and write them at lds_lo,
+// waves 4-7 the upper rows at lds_hi (equal to lds_lo + BYTES/2 for a contiguous block, or a
+// separate half-block buffer).
+template <int D, int BLK>
+__device__ __forceinline__ void issue_block8(const DmaPlan8<D, BLK>& plan, const __bf16* xh,
+                                             uint32_t lds_lo, uint32_t lds_hi, int kb, int n) {
+  using P = DmaPlan8<D, BLK>;
+  using T = Tile<D, BLK>;
+  kb = __builtin_amdgcn_readfirstlane(kb);
+  const int rows = n - kb * BLK;
+  const void* base = (const void*)(xh + (size_t)kb * BLK * D);
+  const uint32_t dst = plan.wave < 4 ? lds_lo : lds_hi - (uint32_t)(T::BYTES / 2);
+  const uint32_t l0 = __builtin_amdgcn_readfirstlane(dst + (uint32_t)(plan.wave * P::S) * 1024u);
+  if (rows >= BLK) {
+#pragma unroll
+    for (int i = 0; i < P::S; i++) dma16(l0 + i * 1024u, plan.off[i], base);
+  } else {
+#pragma unroll
+    for (int i = 0; i < P::S; i++) dma16(l0 + i * 1024u, plan.offset(i, rows), base);
+  }
+}
+
+// O = O^T / l of a finished row block (rows past the end are not stored), LSE if asked.
+template <int D, int BLK>
+__device__ __forceinline__ void store_rows(const WaveState<D, BLK>& st, __bf16* __restrict__ oh,
+                                           float* __restrict__ lseh, int row, int n, int lane) {
+  using T = Tile<D, BLK>;
+  const int h = lane >> 5;
+  const float lsum = pair_sum(st.l);
+  const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+  if (row < n) {
+    __bf16* dst = oh + (size_t)row * D + 4 * h;
+#pragma unroll
+    for (int dt = 0; dt < T::DT; dt++)
+#pragma unroll
+      for (int a = 0; a < 4; a++) {
+        const f32x4 v = {st.o[dt][4 * a] * inv, st.o[dt][4 * a + 1] * inv,
+                         st.o[dt][4 * a + 2] * inv, st.o[dt][4 * a + 3] * inv};
+        *(bf16x4*)(dst + dt * 32 + 8 * a) = __builtin_convertvector(v, bf16x4);
+      }
+    if (lseh && h == 0)
+      lseh[row] = lsum > 0.0f ? (st.m + __builtin_log2f(lsum)) * 0.69314718055994530942f
+                              : -__builtin_inff();
+  }
+}
+
+// Pops the next work item of the persistent schedule (one lane): from queue `queue` first, then
+// from the others in turn; -1 once every queue is exhausted.  Counters only grow: a value at or
+// past a queue's end is final, so an exhausted queue is recognised with a load and costs no
+// atomic.
+__device__ __forceinline__ int32_t pop_item(int32_t* __restrict__ queues,
+                                            const int32_t* __restrict__ order, int& queue,
+                                            int& exhausted) {
+  while (exhausted < kNumQueues) {
+    const int32_t start = queues[queue], len = queues[queue + 1] - start;
+    int32_t* ctr = &queues[kQueueCounters + queue * kCounterStride];
+    int32_t idx = len;
+    if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < len) idx = atomicAdd(ctr, 1);
+    if (idx < len) return order[start + idx];
+    queue = (queue + 1) % kNumQueues;
+    exhausted++;
+  }
+  return -1;
+}
+
+// Entry i of a pair's block stream: key block in bits 0-12, kept by the first row (bit 13) and
+// by the second row (bit 14).
+constexpr int kEntryRowShift = 13;
+constexpr int kEntryBlockMask = (1 << kEntryRowShift) - 1;
+static_assert(PSA_MAX_BLOCKS <= (1 << kEntryRowShift), "block index fits the entry");
+
+// One work item of the pair engine: this wave's row (query block, -1: none) of one (batch, head)
+// and nu stream entries (SPARSE: in `list`; dense: every block, kept by both rows).  Block i
+// sits in buffer i & 1; after one barrier (its loads, issued a block earlier, have landed and
+// block i - 1 is no longer read) the loads of block i + 1 go out and each row that keeps block
+// i runs it: Q K^T, softmax and P V for each half.
+template <int D, int BLK, bool SPARSE, bool PAD>
+__device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int grp,
+                                             const __bf16* __restrict__ qh,
+                                             const __bf16* __restrict__ kh,
+                                             const __bf16* __restrict__ vh,
+                                             __bf16* __restrict__ oh, float* __restrict__ lseh,
+                                             int n, int my_row, int nu, const uint16_t* list,
+                                             float c, uint8_t (*sk)[Tile<D, BLK>::BYTES],
+                                             uint8_t (*sv)[Tile<D, BLK>::BYTES],
+                                             const uint64_t* masks) {
+  using T = Tile<D, BLK>;
+  using H = Half<D, BLK>;
+  constexpr int HALF = T::BYTES / 2;
+  const int tid = threadIdx.x, lane = tid & 63, gw = (tid >> 6) & 3;
+  const int h = lane >> 5, r32 = lane & 31;
+  const int row = my_row * BLK + gw * 32 + r32;
+
+  WaveState<D, BLK> st;
+  if (my_row >= 0) {
+    const bf16x8* src = (const bf16x8*)(qh + (size_t)min(row, n - 1) * D) + h;
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++) st.q[cc] = src[2 * cc];
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++)
+      st.q[cc] = __builtin_convertvector(__builtin_convertvector(st.q[cc], f32x8) * c, bf16x8);
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++) asm volatile("" ::"v"(st.q[cc]));
+  }
+  st.m = -__builtin_inff();
+  st.l = 0.0f;
+  st.negm = (f32x16){};
+#pragma unroll
+  for (int dt = 0; dt < T::DT; dt++) st.o[dt] = (f32x16){};
+
+  auto entry = [&](int i) {
+    return SPARSE ? (int)__builtin_amdgcn_readfirstlane(list[i]) : (i | (3 << kEntryRowShift));
+  };
+  auto issue = [&](int buf, int kb) {
+    issue_block8<D, BLK>(plan, kh, lds_address(sk[buf]), lds_address(sk[buf]) + HALF, kb, n);
+    issue_block8<D, BLK>(plan, vh, lds_address(sv[buf]), lds_address(sv[buf]) + HALF, kb, n);
+  };
+  int e = 0;
+  if (nu > 0) {
+    e = entry(0);
+    issue(0, e & kEntryBlockMask);
+  }
+  for (int i = 0; i < nu; i++) {
+    const int kb = e & kEntryBlockMask;
+    const bool mine = my_row >= 0 && ((e >> (kEntryRowShift + grp)) & 1);
+    uint64_t lo = ~0ull, hi = ~0ull;
+    bool tail;
+    if constexpr (PAD) {
+      lo = masks[2 * kb];
+      hi = masks[2 * kb + 1];
+      tail = (lo & hi) != ~0ull;
+    } else {
+      tail = (kb + 1) * BLK > n;
+    }
+    wait_dma<0>();                                        // block i, issued a block ago
+    __syncthreads();                                      // ... by every wave; block i-1 read
+    if (i + 1 < nu) {
+      e = entry(i + 1);
+      issue((i + 1) & 1, e & kEntryBlockMask);
+    }
+    if (mine) {
+      const uint8_t* skb = sk[i & 1];
+      const uint8_t* svb = sv[i & 1];
+      f32x16 s[H::KT];
+      qk_half<D, BLK>(st, s, skb, 0, lane);
+      softmax_pv_half<D, BLK, PAD>(st, s, svb, kb, 0, n, tail, lo, hi, lane);
+      qk_half<D, BLK>(st, s, skb, H::HK, lane);
+      softmax_pv_half<D, BLK, PAD>(st, s, svb, kb, H::HK, n, tail, lo, hi, lane);
+    }
+  }
+  if (my_row >= 0) store_rows<D, BLK>(st, oh, lseh, row, n, lane);
+}
+
+// SPARSE: persistent, one workgroup per CU popping pair items from the plan's queues; otherwise
+// dense: one workgroup per pair (2 p, 2 p + 1) of the flattened (batch*head, pair) list,
+// consecutive workgroups of one XCD taking consecutive pairs.
+template <int D, int BLK, bool SPARSE, bool PAD>
+__global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2))) void psa_pair_kernel(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+    __bf16* __restrict__ o, float* __restrict__ lse, const psa_stripe_t* __restrict__ params,
+    const int2* __restrict__ coords, const int32_t* __restrict__ order,
+    int32_t* __restrict__ queues, const uint64_t* __restrict__ masks,
+    const int2* __restrict__ pairs, const PlanHeader* __restrict__ header, PlanHeader expect,
+    float c) {
+  using T = Tile<D, BLK>;
+  static_assert(T::kWaves == 4, "a row is four waves");
+  __shared__ __attribute__((aligned(1024))) uint8_t sk[2][T::BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t sv[2][T::BYTES];
+  __shared__ uint16_t list[SPARSE ? PSA_MAX_BLOCKS : 1];
+  __shared__ int32_t misc[16];
+
+  if constexpr (SPARSE) {
+    // A workspace without a finished plan for exactly these sizes is left alone.
+    if (!plan_matches(*header, expect)) return;
+  }
+  const int32_t n_heads = expect.n_heads, n = expect.n, nb = expect.nb;
+  const int32_t np = pairs_per_head(nb), n_items = expect.n_bh * np;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int grp = __builtin_amdgcn_readfirstlane(wave >> 2);
+  DmaPlan8<D, BLK> plan;
+  plan.init(__builtin_amdgcn_readfirstlane(wave), lane);
+  int queue = blockIdx.x % kNumQueues, exhausted = 0;
+  for (int round = 0;; round++) {
+    int32_t item;
+    if constexpr (SPARSE) {
+      if (tid == 0) misc[15] = pop_item(queues, order, queue, exhausted);
+      __syncthreads();
+      item = __builtin_amdgcn_readfirstlane(misc[15]);
+      if (item < 0) break;
+    } else {
+      if (round > 0) break;
+      const int32_t per_xcd = gridDim.x / kNumQueues;
+      item = (blockIdx.x % kNumQueues) * per_xcd + blockIdx.x / kNumQueues;
+      if (item >= n_items) break;
+    }
+    const int32_t bh = item / np, p = item - bh * np, h = bh % n_heads;
+    int2 pr;
+    if constexpr (SPARSE) {
+      pr = pairs[(int64_t)h * np + p];
+    } else {
+      pr = make_int2(2 * p, 2 * p + 1 < nb ? 2 * p + 1 : -1);
+    }
+    const int my_row = __builtin_amdgcn_readfirstlane(grp == 0 ? pr.x : pr.y);
+
+    int32_t nu = nb;
+    if constexpr (SPARSE) {
+      // In-kernel decode of the union of the two rows' kept key blocks (ascending).
+      const psa_stripe_t m = params[h];
+      const int2 ca = coords[pr.x];
+      const int2 cb = pr.y >= 0 ? coords[pr.y] : make_int2(kDeadTile, 0);
+      nu = 0;
+      for (int32_t base = 0; base < nb; base += 8 * 64) {
+        const int32_t kb = base + tid;
+        const int2 ck = kb < nb ? coords[kb] : make_int2(kDeadTile, 0);
+        const bool ka = tile_keep(m, ca, ck), kbk = tile_keep(m, cb, ck);
+        const bool keep = ka || kbk;
+        const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
+        if (lane == 0) misc[wave] = __builtin_popcountll(mask);
+        __syncthreads();
+        int32_t pos = nu, total = 0;
+#pragma unroll
+        for (int w = 0; w < 8; w++) {
+          pos += w < wave ? misc[w] : 0;
+          total += misc[w];
+        }
+        pos += __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                         __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+        if (keep)
+          list[pos] = (uint16_t)(kb | ((ka ? 1 : 0) << kEntryRowShift) | ((kbk ? 1 : 0) << (kEntryRowShift + 1)));
+        nu += total;
+        __syncthreads();
+      }
+    }
+    const size_t off = (size_t)bh * n * D;
+    process_pair<D, BLK, SPARSE, PAD>(plan, grp, q + off, k + off, v + off, o + off,
+                                      lse ? lse + (size_t)bh * n : nullptr, n, my_row, nu, list, c,
+                                      sk, sv, masks);
+  }
+}
+
 template <int D, int BLK, bool PAD>
 static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, void* o,
                                   float* lse, const PlanHeader& expect, float c,
@@ -1267,12 +1732,22 @@ static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, v
                      (const PlanHeader*)(ws + wl.header), expect);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((psa_sparse_kernel<D, BLK, PAD>), dim3(n_wg), dim3(Tile<D, BLK>::kThreads), 0, stream,
-                     (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
-                     (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
-                     (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues),
-                     PAD ? (const uint64_t*)(ws + wl.masks) : nullptr,
-                     (const PlanHeader*)(ws + wl.header), expect, c);
+  if constexpr (BLK == 128) {
+    // one eight-wave pair workgroup per CU
+    hipLaunchKernelGGL((psa_pair_kernel<D, BLK, true, PAD>), dim3(n_wg / 2), dim3(4 * BLK), 0, stream,
+                       (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
+                       (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
+                       (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues),
+                       PAD ? (const uint64_t*)(ws + wl.masks) : nullptr, (const int2*)(ws + wl.pairs),
+                       (const PlanHeader*)(ws + wl.header), expect, c);
+  } else {
+    hipLaunchKernelGGL((psa_sparse_kernel<D, BLK, PAD>), dim3(n_wg), dim3(Tile<D, BLK>::kThreads), 0, stream,
+                       (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
+                       (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
+                       (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues),
+                       PAD ? (const uint64_t*)(ws + wl.masks) : nullptr,
+                       (const PlanHeader*)(ws + wl.header), expect, c);
+  }
   return hipGetLastError();
 }
 
@@ -1307,11 +1782,24 @@ template <int D, int BLK>
 static hipError_t launch_dense_t(const void* q, const void* k, const void* v, void* o, float* lse,
                                  int32_t n_bh, int32_t n, float c, hipStream_t stream) {
   const int32_t nb = (n + BLK - 1) / BLK;
-  const int32_t n_items = n_bh * nb;
-  const int32_t per_xcd = (n_items + kNumQueues - 1) / kNumQueues;
-  hipLaunchKernelGGL((psa_dense_kernel<D, BLK>), dim3(per_xcd * kNumQueues), dim3(Tile<D, BLK>::kThreads), 0, stream,
-                     (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse, n, nb,
-                     n_items, c);
+  if constexpr (BLK == 128) {
+    PlanHeader e = {};
+    e.n_bh = n_bh;
+    e.n_heads = n_bh;
+    e.nb = nb;
+    e.n = n;
+    const int32_t n_items = n_bh * pairs_per_head(nb);
+    const int32_t per_xcd = (n_items + kNumQueues - 1) / kNumQueues;
+    hipLaunchKernelGGL((psa_pair_kernel<D, BLK, false, false>), dim3(per_xcd * kNumQueues), dim3(4 * BLK), 0,
+                       stream, (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
+                       nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, e, c);
+  } else {
+    const int32_t n_items = n_bh * nb;
+    const int32_t per_xcd = (n_items + kNumQueues - 1) / kNumQueues;
+    hipLaunchKernelGGL((psa_dense_kernel<D, BLK>), dim3(per_xcd * kNumQueues), dim3(Tile<D, BLK>::kThreads), 0, stream,
+                       (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse, n, nb,
+                       n_items, c);
+  }
   return hipGetLastError();
 }
 

@@ -71,9 +71,15 @@ struct WorkspaceLayout {
   size_t counts;    // int32 [batch*n_heads*nb]: kept key blocks per work item
   size_t order;     // int32 [batch*n_heads*nb]: work items in schedule order
   size_t queues;    // int32 [kQueueWords]: queue boundaries and pop counters
+  size_t sigs;      // uint64 [n_heads][nb]: signature of each query block's kept set
+  size_t pairs;     // int2 [n_heads][ceil(nb/2)]: query blocks paired into one work item
   size_t masks;     // uint64 [nb][2]: valid positions of each tile (3D only)
   size_t total;
 };
+
+// Query blocks of one head processed together by the pair engine (BLK = 128): ceil(nb / 2)
+// pairs per head, the second member -1 for a single.
+__host__ __device__ inline int32_t pairs_per_head(int32_t nb) { return (nb + 1) / 2; }
 
 WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb, bool masks);
 

@@ -26,7 +26,7 @@ def write_counters(path, rows):
 
 
 def test_counter_summary_scales_by_the_copy(tmp_path):
-    k = "void psa::psa_sparse_kernel<128, 128, false>(...)"
+    k = "void psa::psa_pair_kernel<128, 128, true, false>(...)"
     write_counters(tmp_path / "f", [("__amd_rocclr_copyBuffer", "FETCH_SIZE", 524288), (k, "FETCH_SIZE", 1000),
                                     (k, "FETCH_SIZE", 3000)])
     write_counters(tmp_path / "w", [("__amd_rocclr_copyBuffer", "WRITE_SIZE", 1048576), (k, "WRITE_SIZE", 10)])
@@ -55,17 +55,22 @@ def test_kernel_table_and_utilisation(tmp_path):
         w = csv.DictWriter(f, fieldnames=["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs",
                                           "MaxNs"])
         w.writeheader()
-        w.writerow({"Name": "void psa::psa_dense_kernel<128, 128>(x)", "Calls": 2, "TotalDurationNs": 2e8,
+        w.writerow({"Name": "void psa::psa_pair_kernel<128, 128, false, false>(x)", "Calls": 2, "TotalDurationNs": 2e8,
                     "AverageNs": 1e8, "Percentage": 100.0, "MinNs": 1e8, "MaxNs": 1e8})
     table = bench.kernel_stats_table(str(trace))
-    assert "| psa::psa_dense_kernel<128, 128> | 2 | 200000.0 | 100000.0 |" in table
-    k = "void psa::psa_dense_kernel<128, 128>(x)"
+    assert "| psa::psa_pair_kernel<128, 128, false, false> | 2 | 200000.0 | 100000.0 |" in table
+    k = "void psa::psa_pair_kernel<128, 128, false, false>(x)"
     cyc = 1.9e8                                   # per XCD: 1.9 GHz over 0.1 s
     write_counters(tmp_path / "sq", [(k, "GRBM_GUI_ACTIVE", 8 * cyc), (k, "SQ_VALU_MFMA_BUSY_CYCLES", 0.5 * cyc * 1024),
                                      (k, "SQ_INSTS_MFMA", 0.5 * cyc * 1024 / 32), (k, "SQ_INSTS_VALU", cyc * 64),
                                      (k, "SQ_ACTIVE_INST_VALU", 0.1 * cyc * 256), (k, "SQ_LDS_BANK_CONFLICT", 0)])
     write_counters(tmp_path / "tcc", [(k, "TCC_HIT_sum", 90), (k, "TCC_MISS_sum", 10)])
-    row = bench.utilisation_rows(str(tmp_path / "sq"), str(tmp_path / "tcc"), str(trace), "x")[0]
+    # the plan's pairing kernels share the prefix of the pair engine but are not attention
+    write_counters(tmp_path / "sq" / "plan", [("void psa::psa_pairing_kernel(x)", "SQ_INSTS_MFMA", 0),
+                                              ("void psa::psa_paircount_kernel(x)", "SQ_INSTS_MFMA", 0)])
+    rows = bench.utilisation_rows(str(tmp_path / "sq"), str(tmp_path / "tcc"), str(trace), "x")
+    assert len(rows) == 1
+    row = rows[0]
     cells = [c.strip() for c in row.strip("|").split("|")]
     assert cells[2:6] == ["100.00", "1.90", "0.500", "32.0"] and cells[-1] == "0.900"
 
@@ -77,9 +82,9 @@ def test_hbm_and_wait_summaries(tmp_path):
         w = csv.DictWriter(f, fieldnames=["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs",
                                           "MaxNs"])
         w.writeheader()
-        w.writerow({"Name": "void psa::psa_sparse_kernel<128, 128, false>(x)", "Calls": 1, "TotalDurationNs": 1e7,
+        w.writerow({"Name": "void psa::psa_pair_kernel<128, 128, true, false>(x)", "Calls": 1, "TotalDurationNs": 1e7,
                     "AverageNs": 1e7, "Percentage": 100.0, "MinNs": 1e7, "MaxNs": 1e7})
-    k = "void psa::psa_sparse_kernel<128, 128, false>(x)"
+    k = "void psa::psa_pair_kernel<128, 128, true, false>(x)"
     write_counters(tmp_path / "f", [("__amd_rocclr_copyBuffer", "FETCH_SIZE", 524288), (k, "FETCH_SIZE", 1e6)])
     write_counters(tmp_path / "w", [("__amd_rocclr_copyBuffer", "WRITE_SIZE", 1048576), (k, "WRITE_SIZE", 1e4)])
     cfg = get_config("tiny")
