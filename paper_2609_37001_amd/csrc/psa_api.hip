@@ -231,7 +231,9 @@ int32_t persistent_workgroups() {
   if (hipGetDevice(&dev) != hipSuccess) return 256;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
     return 256;
-  return 2 * cus;  // two 4-wave workgroups per CU (about 80 KB of LDS each)
+  // Two 4-wave workgroups per CU for the one-row engine (about 80 KB of LDS each); the pair engine
+  // (block 128) launches half as many 8-wave workgroups, one per CU.
+  return 2 * cus;
 }
 
 }  // namespace
