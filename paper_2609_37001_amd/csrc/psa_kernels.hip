@@ -3,13 +3,17 @@
 // Kernels
 //   psa_blockmap_kernel / psa_rowcount_kernel  block map and kept counts (Algorithm 1 per block)
 //   psa_setup_kernel                           stripe parameters and block coordinates -> workspace
-//   psa_count_kernel                           kept key blocks of every (batch, head, query block)
+//   psa_count_kernel                           kept key blocks of every (batch, head, query block),
+//                                              and kept-set signatures for the pairing
+//   psa_pairing_kernel / psa_paircount_kernel  pairs of query blocks (block 128) and their work
 //   psa_schedule_kernel                        load-balanced work order split over 8 XCD queues
-//   psa_sparse_kernel                          persistent block-sparse attention (Algorithm 2)
-//   psa_dense_kernel                           the same tile engine with every block kept
+//   psa_pair_kernel                            block 128: persistent block-sparse attention
+//                                              (Algorithm 2) on pairs of query blocks, or dense
+//   psa_sparse_kernel / psa_dense_kernel       block 64: the same with one query block per item
 //
-// Tile engine (one workgroup of BLK/32 wave64s per query block of BLK rows, head dim D; two
-// workgroups per CU, so two waves share each SIMD):
+// Tile engine (per wave; at block 64 one workgroup of BLK/32 wave64s per query block of BLK rows
+// and two workgroups per CU, at block 128 one eight-wave workgroup per CU on a pair of query
+// blocks, so two waves share each SIMD either way; head dim D):
 //   * every wave owns 32 query rows of the query block and all BLK keys of each key/value
 //     block; lane l holds row l & 31, lanes l and l ^ 32 split its keys.  A block is processed
 //     in two halves of BLK/2 keys, each with its own online-softmax update.
@@ -19,10 +23,12 @@
 //     layout of the next product: P^T needs no data movement.
 //   * O^T += V^T P^T: V stays row-major in LDS and the A operand is assembled with the gfx950 LDS
 //     transpose read (ds_read_b64_tr_b16).
-//   * One K and one V buffer per workgroup, filled by direct global->LDS 16-byte loads
-//     (global_load_lds_dwordx4) by halves: each half of the next block is issued as soon as the
-//     last reader of that half of the current block has passed a barrier.  16-byte chunks are
-//     XOR-swizzled per row so both the K reads and the transposed V reads are bank-conflict free.
+//   * K and V fill LDS by direct global->LDS 16-byte loads (global_load_lds_dwordx4).  Block 64:
+//     one K and one V buffer per workgroup, loaded by halves, each half of the next block issued
+//     as soon as the last reader of that half of the current block has passed a barrier.
+//     Block 128: a double buffer shared by the two query blocks of a pair, one barrier per
+//     block.  16-byte chunks are XOR-swizzled per row so both the K reads and the transposed V
+//     reads are bank-conflict free.
 //   * Softmax in the exp2 domain: Q is multiplied by scale*log2(e) once, and the S^T
 //     accumulators start at -m, so the MFMAs deliver the exponent directly; the running max is
 //     raised lazily (only when a new max exceeds it by more than 8, i.e. P <= 2^8), which is
