@@ -29,7 +29,9 @@
  *    PSA_ERR_INVALID.
  *  - Every call only enqueues work on `stream` (0 = the null stream of the current device) and
  *    returns; results are ready after the caller synchronises that stream.  The current device
- *    must be the stream's device.
+ *    must be the stream's device.  What a call enqueues is kernels only (no memset, copy,
+ *    allocation or synchronisation), so a caller may capture it in a HIP graph and replay it;
+ *    a replay reads the buffers and, for a run, the plan the captured call was given.
  *  - Arguments are validated before anything is enqueued: on PSA_ERR_INVALID,
  *    PSA_ERR_UNSUPPORTED or PSA_ERR_WORKSPACE no output byte is written.  PSA_ERR_HIP reports a
  *    failed HIP call (launch); psa_last_error() then holds the HIP message.
