@@ -161,12 +161,23 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
                                void* workspace, size_t workspace_bytes, float* lse,
                                int32_t* kept_per_row, hipStream_t stream);
 
-/* Dense attention forward with the same tile engine (every block kept): the speedup baseline.
- * Same tensor layout, with N = n_tokens.  At full density psa_attention_fwd returns the same
- * bits as this call. */
+/* Bytes of device workspace psa_dense_fwd can use (a constant: queue bounds and counters). */
+size_t psa_dense_workspace_size(void);
+
+/* Dense attention forward with the same tile engine (every block kept): the speedup baseline
+ * and the attention of the steps that run dense.  Same tensor layout, with N = n_tokens.  At
+ * full density psa_attention_fwd returns the same bits as this call.
+ *   workspace      device, psa_dense_workspace_size() bytes or more, 256-byte aligned, or NULL.
+ *                  With a workspace a small kernel arms per-XCD work queues in it and a
+ *                  persistent grid takes the work items, each workgroup from its own XCD's queue
+ *                  first and then from the others, so XCDs that run at different clocks finish
+ *                  together.  Without one, each XCD gets an equal fixed share.  The output is
+ *                  the same bits either way.  Calls sharing a workspace must not overlap in time.
+ * A workspace that is too small or misaligned is rejected with PSA_ERR_WORKSPACE. */
 psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o, int32_t batch,
                            int32_t n_heads, int32_t head_dim, int32_t n_tokens, int32_t block,
-                           float softmax_scale, float* lse, hipStream_t stream);
+                           float softmax_scale, float* lse, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------------------
  * 3D PSABlocks and 3D padding (Sec. 3.2, "Hardware-Aware Design" and "3D-Padding for Resolution

@@ -25,7 +25,7 @@ from . import _lib
 from ._lib import STRIDE_INF, PsaError  # noqa: F401
 
 __all__ = ["STRIDE_INF", "PsaError", "num_blocks", "workspace_size", "build_blockmap",
-           "attention_fwd", "plan", "run", "dense_fwd", "Workspace", "library_path",
+           "attention_fwd", "plan", "run", "dense_fwd", "dense_workspace_size", "Workspace", "library_path",
            "blocked_tokens", "to_blocks", "from_blocks", "build_blockmap_3d", "plan_3d", "run_3d",
            "attention_fwd_3d", "l2_distance"]
 
@@ -212,8 +212,16 @@ def run(q, k, v, grid, block, workspace, scale=None, out=None, return_lse=False,
     return (o, lse) if return_lse else o
 
 
-def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=None):
-    """Dense attention forward with the same tile engine (the speedup baseline)."""
+def dense_workspace_size():
+    return int(_lib.lib().psa_dense_workspace_size())
+
+
+def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=None, workspace=True):
+    """Dense attention forward with the same tile engine (the speedup baseline).
+
+    workspace: True (default) gives the call a fresh workspace, so that a persistent grid
+    balances the work over the XCDs; a uint8 device tensor of dense_workspace_size() bytes is
+    used as given; None runs the fixed grid (an equal share per XCD).  Same output bits."""
     torch = _torch()
     _check_qkv(q, k, v)
     b, h, n, d = q.shape
@@ -221,9 +229,17 @@ def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=Non
     o = torch.empty_like(q) if out is None else out
     _check_qkv(q, o)
     lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+    if workspace is True:
+        # Allocated on the current stream; a call on another stream keeps it alive until that
+        # stream has consumed it.
+        workspace = torch.empty(dense_workspace_size(), dtype=torch.uint8, device=q.device)
+        if stream is not None:
+            workspace.record_stream(stream)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     with torch.cuda.device(q.device):
         _lib.check(_lib.lib().psa_dense_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, n, int(block),
-                                            scale, _ptr(lse), _stream(stream, q.device)))
+                                            scale, _ptr(lse), _ptr(workspace), ws_bytes,
+                                            _stream(stream, q.device)))
     return (o, lse) if return_lse else o
 
 

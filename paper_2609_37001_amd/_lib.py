@@ -22,7 +22,8 @@ PSA_ERR_WORKSPACE = 3
 PSA_ERR_HIP = 4
 
 EXPORTS = ("psa_num_blocks", "psa_workspace_size", "psa_build_blockmap", "psa_attention_plan",
-           "psa_attention_run", "psa_attention_fwd", "psa_dense_fwd", "psa_blocked_tokens",
+           "psa_attention_run", "psa_attention_fwd", "psa_dense_workspace_size", "psa_dense_fwd",
+           "psa_blocked_tokens",
            "psa_to_blocks", "psa_from_blocks", "psa_build_blockmap_3d", "psa_workspace_size_3d",
            "psa_attention_plan_3d", "psa_attention_run_3d", "psa_l2_workspace_size", "psa_l2_distance",
            "psa_status_string", "psa_last_error")
@@ -85,7 +86,10 @@ def lib():
         L.psa_attention_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, i32,
                                         ctypes.POINTER(Stripe), ctypes.c_float, vp, sz, vp, vp, vp]
         L.psa_attention_fwd.restype = ctypes.c_int
-        L.psa_dense_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, vp, vp]
+        L.psa_dense_workspace_size.argtypes = []
+        L.psa_dense_workspace_size.restype = sz
+        L.psa_dense_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, vp, vp, sz,
+                                    vp]
         L.psa_dense_fwd.restype = ctypes.c_int
         L.psa_blocked_tokens.argtypes = [Grid, Block3d]
         L.psa_blocked_tokens.restype = i64

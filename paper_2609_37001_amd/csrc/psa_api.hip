@@ -419,9 +419,12 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
                            workspace, workspace_bytes, lse, stream);
 }
 
+size_t psa_dense_workspace_size(void) { return psa::kDenseWorkspaceBytes; }
+
 psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o, int32_t batch,
                            int32_t n_heads, int32_t head_dim, int32_t n_tokens, int32_t block,
-                           float softmax_scale, float* lse, hipStream_t stream) {
+                           float softmax_scale, float* lse, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
   psa_status_t s = check_tensors(q, k, v, o, lse);
   if (s != PSA_OK) return s;
   s = check_attention_shape(batch, n_heads, head_dim, block);
@@ -430,8 +433,14 @@ psa_status_t psa_dense_fwd(const void* q, const void* k, const void* v, void* o,
     return fail(PSA_ERR_INVALID, "n_tokens must be in [1, 2^31 - 2*block) (got %d)", n_tokens);
   const int64_t items = (int64_t)batch * n_heads * ((n_tokens + block - 1) / block);
   if (items + 8 >= ((int64_t)1 << 31)) return fail(PSA_ERR_UNSUPPORTED, "too many work items");
+  if (workspace && workspace_bytes < psa::kDenseWorkspaceBytes)
+    return fail(PSA_ERR_WORKSPACE, "dense workspace of %zu bytes; %zu bytes required", workspace_bytes,
+                psa::kDenseWorkspaceBytes);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(PSA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   const float c = softmax_scale * 1.4426950408889634f;
-  hipError_t e = psa::launch_dense(q, k, v, o, lse, batch, n_heads, head_dim, n_tokens, block, c, stream);
+  hipError_t e = psa::launch_dense(q, k, v, o, lse, batch, n_heads, head_dim, n_tokens, block, c,
+                                   (int32_t*)workspace, persistent_workgroups(), stream);
   if (e != hipSuccess) return hip_fail(e, "psa_dense_fwd kernel launch");
   return PSA_OK;
 }

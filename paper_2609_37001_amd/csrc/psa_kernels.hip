@@ -1337,6 +1337,35 @@ __device__ __forceinline__ bool plan_matches(const PlanHeader& h, const PlanHead
          h.pbw == e.pbw;
 }
 
+// Pops the next work item of the persistent schedule (one lane): from queue `queue` first, then
+// from the others in turn; -1 once every queue is exhausted.  Queue x holds list positions
+// queues[x] .. queues[x + 1] - 1 and the item at position i is order[i] (i itself without an
+// order).  Counters only grow: a value at or past a queue's end is final, so an exhausted queue
+// is recognised with a load and costs no atomic.
+__device__ __forceinline__ int32_t pop_item(int32_t* __restrict__ queues,
+                                            const int32_t* __restrict__ order, int& queue,
+                                            int& exhausted) {
+  while (exhausted < kNumQueues) {
+    const int32_t start = queues[queue], len = queues[queue + 1] - start;
+    int32_t* ctr = &queues[kQueueCounters + queue * kCounterStride];
+    int32_t idx = len;
+    if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < len) idx = atomicAdd(ctr, 1);
+    if (idx < len) return order ? order[start + idx] : start + idx;
+    queue = (queue + 1) % kNumQueues;
+    exhausted++;
+  }
+  return -1;
+}
+
+// Arms the queues of a dense call: n_items work items in their natural order, cut into
+// kNumQueues contiguous ranges of (nearly) equal length, counters at zero.
+__global__ __launch_bounds__(64) void psa_dense_arm_kernel(int32_t* __restrict__ queues,
+                                                           int32_t n_items) {
+  const int t = threadIdx.x;
+  if (t <= kNumQueues) queues[t] = (int32_t)((int64_t)n_items * t / kNumQueues);
+  if (t < kNumQueues) queues[kQueueCounters + t * kCounterStride] = 0;
+}
+
 // Re-arms the plan's queue counters before each run (a workspace without a matching plan is
 // left alone).
 __global__ __launch_bounds__(64) void psa_rearm_kernel(int32_t* __restrict__ queues,
@@ -1372,25 +1401,7 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
   plan.init(lds_address(sk), lds_address(sv), __builtin_amdgcn_readfirstlane(wave), lane);
   int queue = blockIdx.x % kNumQueues, exhausted = 0;
   while (true) {
-    if (tid == 0) {
-      int32_t item = -1;
-      while (exhausted < kNumQueues) {
-        const int32_t start = queues[queue], len = queues[queue + 1] - start;
-        int32_t* ctr = &queues[kQueueCounters + queue * kCounterStride];
-        // Counters only grow: a value at or past the end is final, so an exhausted queue is
-        // recognised with a load and costs no atomic.
-        int32_t idx = len;
-        if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < len)
-          idx = atomicAdd(ctr, 1);
-        if (idx < len) {
-          item = order[start + idx];
-          break;
-        }
-        queue = (queue + 1) % kNumQueues;
-        exhausted++;
-      }
-      misc[7] = item;
-    }
+    if (tid == 0) misc[7] = pop_item(queues, order, queue, exhausted);
     __syncthreads();
     const int32_t item = misc[7];
     if (item < 0) break;
@@ -1434,20 +1445,36 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
                                                         const __bf16* __restrict__ v,
                                                         __bf16* __restrict__ o,
                                                         float* __restrict__ lse, int32_t n,
-                                                        int32_t nb, int32_t n_items, float c) {
+                                                        int32_t nb, int32_t n_items,
+                                                        int32_t* __restrict__ queues, float c) {
   using T = Tile<D, BLK>;
   __shared__ __attribute__((aligned(1024))) uint8_t sk[T::BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sv[T::BYTES];
-  const int32_t per_xcd = gridDim.x / kNumQueues;
-  const int32_t item = (blockIdx.x % kNumQueues) * per_xcd + blockIdx.x / kNumQueues;
-  if (item >= n_items) return;
-  const int32_t bh = item / nb, qb = item - bh * nb;
-  const size_t off = (size_t)bh * n * D;
+  __shared__ int32_t next_item;
   DmaPlan<D, BLK> plan;
   plan.init(lds_address(sk), lds_address(sv), __builtin_amdgcn_readfirstlane(threadIdx.x >> 6),
             threadIdx.x & 63);
-  process_item<D, BLK, false>(plan, q + off, k + off, v + off, o + off,
-                              lse ? lse + (size_t)bh * n : nullptr, n, qb, nb, nullptr, c, sk, sv);
+  int queue = blockIdx.x % kNumQueues, exhausted = 0;
+  for (int round = 0;; round++) {
+    int32_t item;
+    if (queues) {
+      // Persistent: items from the armed queues, this XCD's first, then the others'.
+      if (threadIdx.x == 0) next_item = pop_item(queues, nullptr, queue, exhausted);
+      __syncthreads();
+      item = __builtin_amdgcn_readfirstlane(next_item);
+      if (item < 0) break;
+    } else {
+      // One item per workgroup, consecutive workgroups of one XCD on consecutive items.
+      if (round > 0) break;
+      const int32_t per_xcd = gridDim.x / kNumQueues;
+      item = (blockIdx.x % kNumQueues) * per_xcd + blockIdx.x / kNumQueues;
+      if (item >= n_items) break;
+    }
+    const int32_t bh = item / nb, qb = item - bh * nb;
+    const size_t off = (size_t)bh * n * D;
+    process_item<D, BLK, false>(plan, q + off, k + off, v + off, o + off,
+                                lse ? lse + (size_t)bh * n : nullptr, n, qb, nb, nullptr, c, sk, sv);
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1532,25 +1559,6 @@ __device__ __forceinline__ void store_rows(const WaveState<D, BLK>& st, __bf16* 
       lseh[row] = lsum > 0.0f ? (st.m + __builtin_log2f(lsum)) * 0.69314718055994530942f
                               : -__builtin_inff();
   }
-}
-
-// Pops the next work item of the persistent schedule (one lane): from queue `queue` first, then
-// from the others in turn; -1 once every queue is exhausted.  Counters only grow: a value at or
-// past a queue's end is final, so an exhausted queue is recognised with a load and costs no
-// atomic.
-__device__ __forceinline__ int32_t pop_item(int32_t* __restrict__ queues,
-                                            const int32_t* __restrict__ order, int& queue,
-                                            int& exhausted) {
-  while (exhausted < kNumQueues) {
-    const int32_t start = queues[queue], len = queues[queue + 1] - start;
-    int32_t* ctr = &queues[kQueueCounters + queue * kCounterStride];
-    int32_t idx = len;
-    if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < len) idx = atomicAdd(ctr, 1);
-    if (idx < len) return order[start + idx];
-    queue = (queue + 1) % kNumQueues;
-    exhausted++;
-  }
-  return -1;
 }
 
 // Entry i of a pair's block stream: key block in bits 0-12, kept by the first row (bit 13) and
@@ -1641,9 +1649,10 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
   if (my_row >= 0) store_rows<D, BLK>(st, oh, lseh, row, n, lane);
 }
 
-// SPARSE: persistent, one workgroup per CU popping pair items from the plan's queues; otherwise
-// dense: one workgroup per pair (2 p, 2 p + 1) of the flattened (batch*head, pair) list,
-// consecutive workgroups of one XCD taking consecutive pairs.
+// SPARSE: persistent, one workgroup per CU popping pair items from the plan's queues.  Dense: the
+// pairs (2 p, 2 p + 1) of the flattened (batch*head, pair) list, either popped from armed queues
+// by a persistent grid (queues given) or one pair per workgroup, consecutive workgroups of one
+// XCD taking consecutive pairs.
 template <int D, int BLK, bool SPARSE, bool PAD>
 __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2))) void psa_pair_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
@@ -1677,7 +1686,14 @@ __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
       __syncthreads();
       item = __builtin_amdgcn_readfirstlane(misc[15]);
       if (item < 0) break;
+    } else if (queues) {
+      // Dense, persistent: items from the armed queues in their natural order.
+      if (tid == 0) misc[15] = pop_item(queues, nullptr, queue, exhausted);
+      __syncthreads();
+      item = __builtin_amdgcn_readfirstlane(misc[15]);
+      if (item < 0) break;
     } else {
+      // Dense, one item per workgroup, consecutive workgroups of one XCD on consecutive items.
       if (round > 0) break;
       const int32_t per_xcd = gridDim.x / kNumQueues;
       item = (blockIdx.x % kNumQueues) * per_xcd + blockIdx.x / kNumQueues;
@@ -1784,43 +1800,54 @@ hipError_t launch_sparse(const void* q, const void* k, const void* v, void* o, f
   return hipErrorInvalidValue;
 }
 
+// Dense attention.  With queues (a dense workspace) a one-thread-group kernel arms them and a
+// persistent grid of n_wg one-row workgroups (n_wg / 2 pair workgroups) takes the items;
+// without, one workgroup per item.
 template <int D, int BLK>
 static hipError_t launch_dense_t(const void* q, const void* k, const void* v, void* o, float* lse,
-                                 int32_t n_bh, int32_t n, float c, hipStream_t stream) {
+                                 int32_t n_bh, int32_t n, float c, int32_t* queues, int32_t n_wg,
+                                 hipStream_t stream) {
   const int32_t nb = (n + BLK - 1) / BLK;
+  const int32_t n_items = BLK == 128 ? n_bh * pairs_per_head(nb) : n_bh * nb;
+  const int32_t per_xcd = (n_items + kNumQueues - 1) / kNumQueues;
+  if (queues) {
+    hipLaunchKernelGGL(psa_dense_arm_kernel, dim3(1), dim3(64), 0, stream, queues, n_items);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if constexpr (BLK == 128) {
     PlanHeader e = {};
     e.n_bh = n_bh;
     e.n_heads = n_bh;
     e.nb = nb;
     e.n = n;
-    const int32_t n_items = n_bh * pairs_per_head(nb);
-    const int32_t per_xcd = (n_items + kNumQueues - 1) / kNumQueues;
-    hipLaunchKernelGGL((psa_pair_kernel<D, BLK, false, false>), dim3(per_xcd * kNumQueues), dim3(4 * BLK), 0,
-                       stream, (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
-                       nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, e, c);
+    const int32_t grid = queues ? n_wg / 2 : per_xcd * kNumQueues;
+    hipLaunchKernelGGL((psa_pair_kernel<D, BLK, false, false>), dim3(grid), dim3(4 * BLK), 0, stream,
+                       (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse, nullptr,
+                       nullptr, nullptr, queues, nullptr, nullptr, nullptr, e, c);
   } else {
-    const int32_t n_items = n_bh * nb;
-    const int32_t per_xcd = (n_items + kNumQueues - 1) / kNumQueues;
-    hipLaunchKernelGGL((psa_dense_kernel<D, BLK>), dim3(per_xcd * kNumQueues), dim3(Tile<D, BLK>::kThreads), 0, stream,
+    const int32_t grid = queues ? n_wg : per_xcd * kNumQueues;
+    hipLaunchKernelGGL((psa_dense_kernel<D, BLK>), dim3(grid), dim3(Tile<D, BLK>::kThreads), 0, stream,
                        (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse, n, nb,
-                       n_items, c);
+                       n_items, queues, c);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_dense(const void* q, const void* k, const void* v, void* o, float* lse,
                         int32_t batch, int32_t n_heads, int32_t head_dim, int32_t n_tokens,
-                        int32_t block, float c, hipStream_t stream) {
+                        int32_t block, float c, int32_t* queues, int32_t n_workgroups,
+                        hipStream_t stream) {
   const int32_t n_bh = batch * n_heads;
+  const int32_t w = n_workgroups;
   if (head_dim == 128 && block == 128)
-    return launch_dense_t<128, 128>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+    return launch_dense_t<128, 128>(q, k, v, o, lse, n_bh, n_tokens, c, queues, w, stream);
   if (head_dim == 64 && block == 64)
-    return launch_dense_t<64, 64>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+    return launch_dense_t<64, 64>(q, k, v, o, lse, n_bh, n_tokens, c, queues, w, stream);
   if (head_dim == 128 && block == 64)
-    return launch_dense_t<128, 64>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+    return launch_dense_t<128, 64>(q, k, v, o, lse, n_bh, n_tokens, c, queues, w, stream);
   if (head_dim == 64 && block == 128)
-    return launch_dense_t<64, 128>(q, k, v, o, lse, n_bh, n_tokens, c, stream);
+    return launch_dense_t<64, 128>(q, k, v, o, lse, n_bh, n_tokens, c, queues, w, stream);
   return hipErrorInvalidValue;
 }
 

@@ -63,6 +63,9 @@ constexpr int kCounterStride = 32;
 constexpr int kQueueCounters = 32;
 constexpr int kQueueWords = kQueueCounters + kNumQueues * kCounterStride;
 
+// Workspace of psa_dense_fwd: the queue area alone, rounded up to 256 bytes.
+constexpr size_t kDenseWorkspaceBytes = (sizeof(int32_t) * kQueueWords + 255) / 256 * 256;
+
 // Workspace of psa_attention_plan / psa_attention_run (byte offsets, each 256-aligned).
 struct WorkspaceLayout {
   size_t header;    // PlanHeader
@@ -118,8 +121,11 @@ hipError_t launch_sparse(const void* q, const void* k, const void* v, void* o, f
                          float scale_log2, void* workspace, const WorkspaceLayout& wl,
                          int32_t n_workgroups, hipStream_t stream);
 
+// queues: the int32 [kQueueWords] queue area of a dense workspace (persistent grid of
+// n_workgroups one-row workgroups), or nullptr (one workgroup per work item).
 hipError_t launch_dense(const void* q, const void* k, const void* v, void* o, float* lse,
                         int32_t batch, int32_t n_heads, int32_t head_dim, int32_t n_tokens,
-                        int32_t block, float scale_log2, hipStream_t stream);
+                        int32_t block, float scale_log2, int32_t* queues, int32_t n_workgroups,
+                        hipStream_t stream);
 
 }  // namespace psa

@@ -82,11 +82,17 @@ def test_error_messages():
 def test_dense_validation_codes():
     L = _lib.lib()
     vp = ctypes.c_void_p
-    args = lambda n, d, blk, q=256: (vp(q), vp(256), vp(256), vp(256), 1, 1, d, n, blk, 0.1, None, None)
+    args = lambda n, d, blk, q=256, ws=None, wsb=0: (vp(q), vp(256), vp(256), vp(256), 1, 1, d, n, blk, 0.1,
+                                                     None, vp(ws), wsb, None)
     assert L.psa_dense_fwd(*args(0, 128, 128)) == _lib.PSA_ERR_INVALID
     assert L.psa_dense_fwd(*args(100, 48, 128)) == _lib.PSA_ERR_UNSUPPORTED
     assert L.psa_dense_fwd(*args(100, 64, 16)) == _lib.PSA_ERR_UNSUPPORTED
     assert L.psa_dense_fwd(*args(100, 64, 64, q=0)) == _lib.PSA_ERR_INVALID
+    need = L.psa_dense_workspace_size()
+    assert need >= 8 * 4 and need % 256 == 0
+    assert L.psa_dense_fwd(*args(100, 64, 64, ws=512, wsb=need - 1)) == _lib.PSA_ERR_WORKSPACE
+    assert L.psa_dense_fwd(*args(100, 64, 64, ws=512 + 128, wsb=need)) == _lib.PSA_ERR_WORKSPACE
+    assert b"aligned" in L.psa_last_error()
 
 
 def test_blockmap_validation_codes():
@@ -221,7 +227,7 @@ def test_misaligned_pointers_are_rejected():
     assert run(o=258) == _lib.PSA_ERR_INVALID
     assert run(lse=257) == _lib.PSA_ERR_INVALID
     dense = lambda q=256, lse=None: L.psa_dense_fwd(vp(q), vp(256), vp(256), vp(256), 1, 1, 128, 256, 128,
-                                                    0.1, vp(lse), None)
+                                                    0.1, vp(lse), None, 0, None)
     assert dense(q=264) == _lib.PSA_ERR_INVALID
     assert dense(lse=258) == _lib.PSA_ERR_INVALID
     b3 = _b3(2, 4, 16)

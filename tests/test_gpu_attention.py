@@ -111,6 +111,21 @@ def test_dense_full(d, block):
     assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
 
 
+@pytest.mark.parametrize("d,block", [(64, 64), (128, 128), (128, 64), (64, 128)])
+def test_dense_persistent_equals_fixed_grid(d, block):
+    """With a workspace the dense call runs a persistent grid over armed per-XCD queues; without
+    one a fixed grid.  Same bits, including a reused workspace on the second call."""
+    torch = gu.torch()
+    n = 5 * block + 37
+    q, k, v = (dev(x) for x in random_problem(2, 3, n, d, seed=d + 3 * block))
+    o_f, l_f = psa.dense_fwd(q, k, v, block, 0.1, return_lse=True, workspace=None)
+    ws = torch.empty(psa.dense_workspace_size(), dtype=torch.uint8, device="cuda:0")
+    for _ in range(2):
+        o_p, l_p = psa.dense_fwd(q, k, v, block, 0.1, return_lse=True, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(o_p, o_f) and torch.equal(l_p, l_f)
+
+
 def test_full_density_sparse_equals_dense_bitwise():
     f, hh, ww = 4, 16, 24
     n = f * hh * ww
