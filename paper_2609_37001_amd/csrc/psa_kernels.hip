@@ -496,12 +496,19 @@ __device__ int32_t block_scan(int32_t* v, int32_t n, int32_t* part) {
 
 // One workgroup per head: pairs of query blocks for the pair engine.  The rows are sorted by the
 // signature of their kept set (then by index); within a run of equal signatures consecutive
-// rows pair up; the rows left over pair up in index order.  pairs[h][p] = (first row, second
-// row or -1), in the order of the first rows.  Rows with equal kept sets share every key block,
-// so most pairs of the stripe patterns waste no work; the pairing only affects speed, the
-// run decodes each row's own kept set.
+// rows pair up.  The rows left over pair up consecutively in one of two orders, chosen from the
+// head's stripes: index order (neighbouring slots of one frame), or slot-major (one slot in
+// neighbouring frames) where a one-frame shift widens the kept set less than a one-slot shift.
+// A shift by one position grows an axis' kept set by (w + 1) / w for a stripe narrower than its
+// stride and leaves a full axis unchanged, so slot-major is taken when the spatial stripes are
+// partial and the temporal ones either cover their axis or are wider (T_w > S_w).
+// pairs[h][p] = (first row, second row or -1), in the order of the first rows.  Rows with
+// equal kept sets share every key block, so most pairs of the stripe patterns waste no work;
+// the pairing only affects speed, the run decodes each row's own kept set.
 constexpr int kPairSort = 8192;                 // a power of two >= PSA_MAX_BLOCKS
 __global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __restrict__ sigs,
+                                                           const psa_stripe_t* __restrict__ params,
+                                                           const int2* __restrict__ coords,
                                                            int2* __restrict__ pairs, int32_t nb) {
   __shared__ uint64_t key[kPairSort];         // sorted (signature, row); later leftover rows
   __shared__ int32_t run[kPairSort];          // start of each sorted position's run
@@ -516,20 +523,23 @@ __global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __res
     partner[i] = -3;
   }
   __syncthreads();
-  for (int32_t k = 2; k <= n2; k <<= 1)
-    for (int32_t j = k >> 1; j > 0; j >>= 1) {
-      for (int32_t i = tid; i < n2; i += 1024) {
-        const int32_t ixj = i ^ j;
-        if (ixj > i) {
-          const uint64_t a = key[i], b = key[ixj];
-          if ((a > b) == ((i & k) == 0)) {
-            key[i] = b;
-            key[ixj] = a;
+  auto sort_keys = [&]() {                                // bitonic sort of key[0 .. n2), ascending
+    for (int32_t k = 2; k <= n2; k <<= 1)
+      for (int32_t j = k >> 1; j > 0; j >>= 1) {
+        for (int32_t i = tid; i < n2; i += 1024) {
+          const int32_t ixj = i ^ j;
+          if (ixj > i) {
+            const uint64_t a = key[i], b = key[ixj];
+            if ((a > b) == ((i & k) == 0)) {
+              key[i] = b;
+              key[ixj] = a;
+            }
           }
         }
+        __syncthreads();
       }
-      __syncthreads();
-    }
+  };
+  sort_keys();
   auto row_of = [&](int32_t i) { return (int32_t)(key[i] & 8191u); };
   auto same = [&](int32_t i, int32_t j) { return (key[i] >> 13) == (key[j] >> 13); };
   for (int32_t i = tid; i < nb; i += 1024) run[i] = (i == 0 || !same(i, i - 1)) ? i : -1;
@@ -547,13 +557,48 @@ __global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __res
     }
   }
   __syncthreads();
-  // Leftover rows in index order: rank by a prefix sum over the rows, pair ranks 2k and 2k + 1.
+  // Leftover rows: rank in the chosen order (a prefix sum over the rows gives index order), pair
+  // ranks 2k and 2k + 1.
+  const psa_stripe_t m = params[blockIdx.x];
+  const bool slot_major = m.s_w < m.s_s && (m.t_w >= m.t_s || m.t_w > m.s_w);
   for (int32_t i = tid; i < nb; i += 1024) run[i] = partner[i] == -4 ? 1 : 0;
   __syncthreads();
   const int32_t n_left = block_scan<false>(run, nb, part);
   uint32_t* left = (uint32_t*)key;                        // rank -> row
-  for (int32_t i = tid; i < nb; i += 1024)
-    if (partner[i] == -4) left[run[i]] = (uint32_t)i;
+  if (!slot_major) {
+    for (int32_t i = tid; i < nb; i += 1024)
+      if (partner[i] == -4) left[run[i]] = (uint32_t)i;
+  } else {
+    // Sort the leftover rows by (slot, frame, row); other rows sort last.  Coordinates beyond
+    // the fields (global and padding blocks have negative frames) are clamped: any order is a
+    // valid pairing.
+    for (int32_t i = tid; i < n2; i += 1024) {
+      uint64_t kk = ~0ull;
+      if (i < nb && partner[i] == -4) {
+        const int2 c = coords[i];
+        kk = ((uint64_t)min((uint32_t)c.y, (1u << 26) - 1) << 38) |
+             ((uint64_t)min((uint32_t)c.x, (1u << 25) - 1) << 13) | (uint64_t)i;
+      }
+      key[i] = kk;
+    }
+    __syncthreads();
+    sort_keys();
+    // left[] overlays key[]: every thread reads its sorted rows before any is written.
+    uint32_t rows[kPairSort / 1024];
+#pragma unroll
+    for (int j = 0; j < kPairSort / 1024; j++) {
+      const int32_t r = tid + 1024 * j;
+      rows[j] = r < n_left ? (uint32_t)(key[r] & 8191u) : 0u;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kPairSort / 1024; j++) {
+      const int32_t r = tid + 1024 * j;
+      if (r < n_left) left[r] = rows[j];
+    }
+    __syncthreads();
+    for (int32_t r = tid; r < n_left; r += 1024) run[left[r]] = r;
+  }
   __syncthreads();
   for (int32_t i = tid; i < nb; i += 1024)
     if (partner[i] == -4) {
@@ -878,7 +923,7 @@ hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, vo
                        nullptr, kept_per_row, (uint64_t*)(ws + wl.sigs), n_rows, n_heads, g.nb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(psa_pairing_kernel, dim3(n_heads), dim3(1024), 0, stream,
-                       (const uint64_t*)(ws + wl.sigs), (int2*)(ws + wl.pairs), g.nb);
+                       (const uint64_t*)(ws + wl.sigs), params, coords, (int2*)(ws + wl.pairs), g.nb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     per_head = pairs_per_head(g.nb);
     const int32_t n_items = batch * n_heads * per_head;
