@@ -216,12 +216,14 @@ def dense_workspace_size():
     return int(_lib.lib().psa_dense_workspace_size())
 
 
-def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=None, workspace=True):
+def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=None, workspace=None,
+              balanced=True):
     """Dense attention forward with the same tile engine (the speedup baseline).
 
-    workspace: True (default) gives the call a fresh workspace, so that a persistent grid
-    balances the work over the XCDs; a uint8 device tensor of dense_workspace_size() bytes is
-    used as given; None runs the fixed grid (an equal share per XCD).  Same output bits."""
+    balanced (default): a persistent grid takes the work items from per-XCD queues in a small
+    workspace -- `workspace`, a uint8 device tensor of dense_workspace_size() bytes, or a fresh
+    one -- so that XCDs holding different clocks finish together.  balanced=False runs the fixed
+    grid (an equal share per XCD, no workspace).  Same output bits either way."""
     torch = _torch()
     _check_qkv(q, k, v)
     b, h, n, d = q.shape
@@ -229,7 +231,9 @@ def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=Non
     o = torch.empty_like(q) if out is None else out
     _check_qkv(q, o)
     lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
-    if workspace is True:
+    if not balanced:
+        workspace = None
+    elif workspace is None:
         # Allocated on the current stream; a call on another stream keeps it alive until that
         # stream has consumed it.
         workspace = torch.empty(dense_workspace_size(), dtype=torch.uint8, device=q.device)

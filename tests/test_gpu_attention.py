@@ -118,7 +118,7 @@ def test_dense_persistent_equals_fixed_grid(d, block):
     torch = gu.torch()
     n = 5 * block + 37
     q, k, v = (dev(x) for x in random_problem(2, 3, n, d, seed=d + 3 * block))
-    o_f, l_f = psa.dense_fwd(q, k, v, block, 0.1, return_lse=True, workspace=None)
+    o_f, l_f = psa.dense_fwd(q, k, v, block, 0.1, return_lse=True, balanced=False)
     ws = torch.empty(psa.dense_workspace_size(), dtype=torch.uint8, device="cuda:0")
     for _ in range(2):
         o_p, l_p = psa.dense_fwd(q, k, v, block, 0.1, return_lse=True, workspace=ws)
