@@ -55,13 +55,15 @@ def test_one_token(d, block):
 
 
 def test_largest_block_count():
-    """nb = PSA_MAX_BLOCKS = 7936 blocks of 128 (62 frames of 128 x 128 tokens, N = 1015808)."""
+    """nb = PSA_MAX_BLOCKS = 7936 blocks of 128 (62 frames of 128 x 128 tokens, N = 1015808).  The
+    first head pairs its leftover query blocks in index order, the second (T_w > S_w) slot-major:
+    the pairing kernel's sorts run at their largest size."""
     f, hh, ww, block = 62, 128, 128, 128
     n = f * hh * ww
     assert psa.num_blocks((f, hh, ww), block) == _lib.MAX_BLOCKS
     rng = np.random.default_rng(5)
-    q, k, v = (bf16_round(rng.standard_normal((1, 1, n, 128)).astype(np.float32)) for _ in range(3))
-    params = [(1, 0, INF, 2, 0, INF)]                             # own frame, neighbouring slots
+    q, k, v = (bf16_round(rng.standard_normal((1, 2, n, 128)).astype(np.float32)) for _ in range(3))
+    params = [(1, 0, INF, 2, 0, INF), (3, 1, INF, 1, 0, 3)]      # own frame / three frames, nearby slots
     o, lse, kept = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww), block, params, 0.09,
                                      return_lse=True, return_kept_per_row=True)
     gu.torch().cuda.synchronize()
@@ -74,9 +76,11 @@ def test_largest_block_count():
                           params, 0.09)
 
 
-def test_largest_batch_heads():
-    """batch x heads = PSA_MAX_BATCH_HEADS = 1024 (4 x 256 heads, each with its own stripes)."""
-    b, h, grid, block, d = 4, 256, (2, 8, 16, 5), 64, 64
+@pytest.mark.parametrize("block,d", [(64, 64), (128, 128)])
+def test_largest_batch_heads(block, d):
+    """batch x heads = PSA_MAX_BATCH_HEADS = 1024 (4 x 256 heads, each with its own stripes); block
+    128 runs the pair engine, one pairing workgroup per head."""
+    b, h, grid = 4, 256, (2, 8, 16, 5)
     n = 2 * 8 * 16 + 5
     rng = np.random.default_rng(9)
     params = [(int(rng.integers(1, 3)), int(rng.choice([0, 1, -1])), int(rng.choice([1, 2, INF])),
