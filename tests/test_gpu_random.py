@@ -1,5 +1,6 @@
 """Seeded random GPU parity cases: random grids (ragged ends, text), random stripe parameters
-from the paper's ranges, every (head_dim, block) variant, batch 1-2; 1D blocks and 3D PSABlocks.
+from the paper's ranges, every (head_dim, block) variant, batch 1-2; 1D blocks, the pair engine with
+both pairing orders of leftover query blocks, and 3D PSABlocks.
 Every output row is compared with the oracle."""
 import numpy as np
 import pytest
@@ -92,4 +93,36 @@ def test_random_3d(seed):
     groups = oracle.token_groups(f, hh, ww, nt, pb)
     rel, mx, mlse = compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse, groups=groups)
     print("seed %d: grid %s pb %s tile %d d %d rel %.2e max %.2e lse %.2e" % (seed, grid, pb, tile, d, rel, mx, mlse))
+    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+
+
+def slot_major(m):
+    """Whether the plan pairs a head's leftover query blocks slot-major (the kernel's rule)."""
+    tw, _, ts, sw, _, ss = m
+    return sw < ss and (tw >= ts or tw > sw)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_pair_engine(seed):
+    """Block 128 (the pair engine) on random grids with heads of both leftover pairing orders
+    (index and slot-major), odd and even block counts, text and batch 1-2."""
+    rng = np.random.default_rng([9, seed])
+    d = int(rng.choice([64, 128]))
+    f, hh, ww = int(rng.integers(2, 6)), int(rng.integers(4, 17)), int(rng.integers(8, 48))
+    nt = int(rng.choice([0, int(rng.integers(1, 300))]))
+    n = f * hh * ww + nt
+    sp = -(-(hh * ww) // 128)
+    params = random_params(rng, 2, f, sp)
+    params += [(min(f, 3), 0, INF, 1, 0, 3), (1, 0, INF, min(sp, 2), 0, INF)]   # slot-major, index order
+    b = int(rng.integers(1, 3))
+    scale = float(rng.uniform(0.05, 0.2))
+    q, k, v = (bf16_round(rng.standard_normal((b, len(params), n, d)).astype(np.float32)) for _ in range(3))
+    o, lse, kept = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, nt), 128, params, scale, return_lse=True,
+                                     return_kept_per_row=True)
+    gu.torch().cuda.synchronize()
+    keep = oracle.blockmap(params, f, hh, ww, nt, 128)
+    assert np.array_equal(kept.cpu().numpy(), oracle.kept_per_row(keep))
+    assert any(slot_major(m) for m in params) and not all(slot_major(m) for m in params)
+    rel, mx, mlse = compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse.cpu().numpy(), block=128)
+    print("seed %d: n=%d nb=%d d=%d b=%d rel %.2e max %.2e lse %.2e" % (seed, n, keep.shape[1], d, b, rel, mx, mlse))
     assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
