@@ -168,11 +168,11 @@ def summarise_counters(fetch_dir, write_dir, copy_mb):
         "Commands (repository root, MI355X; one counter pass per run):",
         "",
         "    cd /tmp && export TMPDIR=/tmp && cd -",
-        "    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- "
-        "python3 bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --copy-mb %d" % copy_mb,
-        "    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- "
-        "python3 bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --copy-mb %d" % copy_mb,
-        "    python3 bench.py --counters gpurun_out/pmc_fetch gpurun_out/pmc_write",
+        "    rocprofv3 --pmc FETCH_SIZE --output-format csv -d %s -o run -- "
+        "python3 bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --copy-mb %d" % (fetch_dir, copy_mb),
+        "    rocprofv3 --pmc WRITE_SIZE --output-format csv -d %s -o run -- "
+        "python3 bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --copy-mb %d" % (write_dir, copy_mb),
+        "    python3 bench.py --counters %s %s" % (fetch_dir, write_dir),
         "",
         "| quantity | value |",
         "|---|---|",
