@@ -88,6 +88,9 @@ def parse():
                    help="sparse at every forced density of the sweep workload against one dense run")
     p.add_argument("--search", type=int, default=0, metavar="K",
                    help="time PSA-Search scoring of K candidates per head (all heads per call)")
+    p.add_argument("--gemm-reference", action="store_true",
+                   help="time a plain bf16 16384^3 torch.matmul (hipBLASLt): the chip's sustained "
+                        "bf16 MFMA rate under its power limit, for comparison")
     p.add_argument("--kernel-stats", metavar="TRACE_DIR",
                    help="print the kernel table of a rocprofv3 --kernel-trace --stats csv run and exit")
     p.add_argument("--utilisation", nargs=3, metavar=("SQ_DIR", "TCC_DIR", "TRACE_DIR"),
@@ -566,6 +569,24 @@ def bench_sweep(args, torch, psa):
     return 0
 
 
+def bench_gemm_reference(args, torch):
+    """A reference point for the roofline: a plain bf16 16384^3 matrix product through torch
+    (hipBLASLt) on random N(0,1) operands, the chip's sustained dense bf16 MFMA rate under the
+    same power limit as the attention kernels.  Not part of the attention path."""
+    n = 16384
+    gen = torch.Generator(device="cuda:0").manual_seed(0)
+    a = torch.randn(n, n, device="cuda:0", generator=gen).bfloat16()
+    b = torch.randn(n, n, device="cuda:0", generator=gen).bfloat16()
+    c = torch.empty(n, n, device="cuda:0", dtype=torch.bfloat16)
+    t = time_calls(lambda: torch.matmul(a, b, out=c), args.steps, args.warmup, torch)
+    tflops = 2.0 * n ** 3 / (t["mean"] * 1e-3) / 1e12
+    log("gemm reference: bf16 %d^3 torch.matmul %.3f ms (median %.3f, min %.3f), %.1f TFLOP/s, %.3f of %.0f"
+        % (n, t["mean"], t["median"], t["min"], tflops, tflops / PEAK_BF16_TFLOPS, PEAK_BF16_TFLOPS))
+    print(json.dumps({"reference": "bf16 %d^3 torch.matmul (hipBLASLt)" % n, "ms": round(t["mean"], 4),
+                      "tflops": round(tflops, 2), "frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4)}), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.kernel_stats:
@@ -589,10 +610,12 @@ def main():
         print("\n".join(hbm_rows(*args.hbm, get_config(args.workload), args.copy_calibration_mb)))
         return 0
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (the attention "
-              "kernel shards over heads; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: there is no multi-GPU path (the attention would "
+              "shard over heads, with one all-to-all before and after). Run with --gpus 1.", file=sys.stderr)
         return 2
     import torch
+    if args.gemm_reference:
+        return bench_gemm_reference(args, torch)
     import paper_2609_37001_amd as psa
     from workloads import get_config, make_qkv, stripe_params
 
