@@ -93,6 +93,11 @@ def parse():
                         "bf16 MFMA rate under its power limit, for comparison")
     p.add_argument("--kernel-stats", metavar="TRACE_DIR",
                    help="print the kernel table of a rocprofv3 --kernel-trace --stats csv run and exit")
+    p.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_OUT"),
+                   help="summarise a rocprofv3 --kernel-trace run of this script (same --steps, "
+                        "--warmup, --dense-steps): per-launch durations of the timed legs only, "
+                        "and the roofline fraction against the JSON line the run printed to BENCH_OUT; "
+                        "then exit")
     p.add_argument("--utilisation", nargs=3, metavar=("SQ_DIR", "TCC_DIR", "TRACE_DIR"),
                    help="print utilisation figures of the attention kernels from two rocprofv3 "
                         "--pmc runs and a kernel trace, and exit")
@@ -210,6 +215,70 @@ def kernel_stats_table(trace_dir):
                 name, r["Calls"], float(r["TotalDurationNs"]) / 1e3, float(r["AverageNs"]) / 1e3,
                 float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
     return "\n".join(lines) + "\n"
+
+
+def trace_dispatches(trace_dir):
+    """{kernel name: [duration ns in dispatch order]} from rocprofv3's kernel_trace.csv."""
+    paths = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if not paths:
+        raise SystemExit("no kernel_trace.csv under %s" % trace_dir)
+    rows = []
+    with open(paths[0]) as f:
+        for r in csv.DictReader(f):
+            name = r["Kernel_Name"].split("(")[0].replace("void ", "").replace("psa::", "")
+            rows.append((int(r["Dispatch_Id"]), name, int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    out = {}
+    for _, name, ns in sorted(rows):
+        out.setdefault(name, []).append(ns)
+    return out
+
+
+def trace_summary(trace_dir, bench_out, steps, warmup, dense_steps):
+    """The kernel launches of each timed leg of a profiled `bench.py` run (the order of main()):
+    `warmup` + `steps` psa_attention_fwd calls, then 1 + `steps` psa_attention_run calls, then
+    1 + `dense_steps` dense calls; warm-up launches are dropped.  The roofline fraction from the
+    trace's mean of the timed run-alone launches is set beside the one the run's JSON line
+    reports (HIP events around the same launches)."""
+    disp = trace_dispatches(trace_dir)
+    sparse = disp.get(KERNEL.replace("psa::", ""), [])
+    dense = disp.get(KERNEL.replace("true, false", "false, false"), [])
+    expect = warmup + steps + 1 + steps
+    if len(sparse) != expect:
+        raise SystemExit("%d sparse launches in the trace, %d expected from --steps %d --warmup %d"
+                         % (len(sparse), expect, steps, warmup))
+    step_leg = sparse[warmup:warmup + steps]
+    run_leg = sparse[warmup + steps + 1:]
+    dense_leg = dense[1:1 + dense_steps] if len(dense) == 1 + dense_steps else []
+    line = None
+    with open(bench_out) as f:
+        for l in f:
+            if l.startswith("{") and '"roofline"' in l:
+                line = json.loads(l)
+    if line is None:
+        raise SystemExit("no JSON line in %s" % bench_out)
+    flops = line["config"]["computed_tflop"] * 1e12
+    stat = lambda v: (sum(v) / len(v) / 1e6, float(np.median(v)) / 1e6, min(v) / 1e6) if v else (0, 0, 0)
+    s_mean, s_med, s_min = stat(step_leg)
+    r_mean, r_med, r_min = stat(run_leg)
+    d_mean, d_med, d_min = stat(dense_leg)
+    frac_trace = flops / (r_mean * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+    frac_line = line["roofline"]["frac"]
+    rows = [
+        "| leg | launches | mean ms | median ms | min ms |",
+        "|---|---|---|---|---|",
+        "| %s in the timed psa_attention_fwd steps | %d | %.3f | %.3f | %.3f |" % (KERNEL, len(step_leg), s_mean, s_med, s_min),
+        "| %s in the timed psa_attention_run calls (roofline) | %d | %.3f | %.3f | %.3f |" % (KERNEL, len(run_leg), r_mean, r_med, r_min),
+    ]
+    if dense_leg:
+        rows.append("| %s, timed dense calls | %d | %.3f | %.3f | %.3f |"
+                    % (KERNEL.replace("true, false", "false, false"), len(dense_leg), d_mean, d_med, d_min))
+    text = "\n".join(rows) + "\n\n"
+    text += ("Warm-up launches dropped: %d + 1 sparse, 1 dense.  The same run's JSON line: ms_per_step %.4f, "
+             "kernel_ms mean %.4f, roofline frac %.4f.  From the trace: %.4f TFLOP / %.4f ms / %.0f TFLOP/s "
+             "= frac %.4f (%+.2f %% against the line).\n"
+             % (warmup, line["ms_per_step"], line["kernel_ms"]["mean"], frac_line, flops / 1e12, r_mean,
+                PEAK_BF16_TFLOPS, frac_trace, 100.0 * (frac_trace / frac_line - 1.0)))
+    return text
 
 
 def utilisation_rows(sq_dir, tcc_dir, trace_dir, label):
@@ -592,6 +661,10 @@ def main():
     if args.kernel_stats:
         sys.stdout.write(kernel_stats_table(args.kernel_stats))
         return 0
+    if args.trace_summary:
+        sys.stdout.write(trace_summary(args.trace_summary[0], args.trace_summary[1], args.steps, args.warmup,
+                                       args.dense_steps or max(3, args.steps // 2)))
+        return 0
     if args.utilisation:
         label = os.path.basename(os.path.normpath(args.utilisation[0]))
         print(UTIL_HEADER)
@@ -678,8 +751,8 @@ def main():
                    "dense_tflop": round(dense_flops / 1e12, 4)},
         "mfu": round(tflops / PEAK_BF16_TFLOPS, 4),
         "dense_equiv_tflops": round(dense_flops / (ms * 1e-3) / 1e12, 2),
-        "context_paper": "H100, FA3 baseline, uniform 75 %% sparsity at this shape: PSA 55.12 ms, "
-                         "29.26 TFLOP, 53.68 %% MFU (989 TFLOP/s peak); context only, other hardware "
+        "context_paper": "H100, FA3 baseline, uniform 75 % sparsity at this shape: PSA 55.12 ms, "
+                         "29.26 TFLOP, 53.68 % MFU (989 TFLOP/s peak); context only, other hardware "
                          "and workload" if name == "wan14b" else None,
         "step_ms": {key: round(val, 4) for key, val in t_step.items()},
         "kernel_ms": {key: round(val, 4) for key, val in t_kernel.items()},

@@ -19,6 +19,7 @@ is no CPU or PyTorch fallback.
     ob = attention_fwd_3d(qb, kb, vb, grid, pb, params, tile=128)
     o = from_blocks(ob, grid, pb)
 """
+import contextlib
 import math
 
 from . import _lib
@@ -61,6 +62,14 @@ def _stream(stream, device):
     if stream is None:
         stream = torch.cuda.current_stream(device)
     return ctypes_void(stream.cuda_stream)
+
+
+def _on(stream):
+    """Context for the allocations and the library call of one binding function: with a stream
+    given, it becomes torch's current stream, so the tensors the function allocates (outputs,
+    workspaces) belong to that stream's memory pool and are not handed to other work while the
+    library still uses them there.  The caller orders the inputs onto that stream."""
+    return contextlib.nullcontext() if stream is None else _torch().cuda.stream(stream)
 
 
 def ctypes_void(x):
@@ -127,12 +136,12 @@ def build_blockmap(params, grid, block, device=None, blockmap=True, per_row=True
     nb = num_blocks(grid, block)
     if nb < 0:
         raise ValueError("invalid grid or block")
-    bm = torch.empty((heads, nb, nb), dtype=torch.uint8, device=device) if blockmap else None
-    pr = torch.empty((heads, nb), dtype=torch.int32, device=device) if per_row else None
-    ph = torch.empty((heads,), dtype=torch.int64, device=device) if per_head else None
-    with torch.cuda.device(device):
+    with torch.cuda.device(device), _on(stream):
+        bm = torch.empty((heads, nb, nb), dtype=torch.uint8, device=device) if blockmap else None
+        pr = torch.empty((heads, nb), dtype=torch.int32, device=device) if per_row else None
+        ph = torch.empty((heads,), dtype=torch.int64, device=device) if per_head else None
         _lib.check(_lib.lib().psa_build_blockmap(_lib.stripes(params), heads, _grid(grid), int(block),
-                                                 _ptr(bm), _ptr(pr), _ptr(ph), _stream(stream, device)))
+                                                 _ptr(bm), _ptr(pr), _ptr(ph), _stream(None, device)))
     return bm, pr, ph
 
 
@@ -148,17 +157,17 @@ def attention_fwd(q, k, v, grid, block, params, scale=None, out=None, return_lse
         raise ValueError("one stripe tuple per head is required")
     _check_tokens(n, grid)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    o = torch.empty_like(q) if out is None else out
-    _check_qkv(q, o)
-    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
     nb = num_blocks(grid, block)
-    kept = torch.empty((h, max(nb, 1)), dtype=torch.int32, device=q.device) if return_kept_per_row else None
-    ws = workspace if workspace is not None else Workspace(b, h, grid, block, q.device)
-    with torch.cuda.device(q.device):
+    with torch.cuda.device(q.device), _on(stream):
+        o = torch.empty_like(q) if out is None else out
+        _check_qkv(q, o)
+        lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+        kept = torch.empty((h, max(nb, 1)), dtype=torch.int32, device=q.device) if return_kept_per_row else None
+        ws = workspace if workspace is not None else Workspace(b, h, grid, block, q.device)
         _lib.check(_lib.lib().psa_attention_fwd(
             _ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, _grid(grid), int(block),
             _lib.stripes(params), scale, _ptr(ws.tensor), ws.nbytes, _ptr(lse), _ptr(kept),
-            _stream(stream, q.device)))
+            _stream(None, q.device)))
     ws.sizes = (b, h, _grid_tuple(grid), int(block))
     ws.params = [tuple(int(x) for x in m) for m in params]
     res = (o,)
@@ -177,13 +186,13 @@ def plan(params, grid, block, batch=1, device=None, workspace=None, return_kept_
     torch = _torch()
     device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
     h = len(params)
-    ws = workspace if workspace is not None else Workspace(batch, h, grid, block, device)
     nb = num_blocks(grid, block)
-    kept = torch.empty((h, max(nb, 1)), dtype=torch.int32, device=device) if return_kept_per_row else None
-    with torch.cuda.device(device):
+    with torch.cuda.device(device), _on(stream):
+        ws = workspace if workspace is not None else Workspace(batch, h, grid, block, device)
+        kept = torch.empty((h, max(nb, 1)), dtype=torch.int32, device=device) if return_kept_per_row else None
         _lib.check(_lib.lib().psa_attention_plan(int(batch), h, _grid(grid), int(block),
                                                  _lib.stripes(params), _ptr(ws.tensor), ws.nbytes,
-                                                 _ptr(kept), _stream(stream, device)))
+                                                 _ptr(kept), _stream(None, device)))
     ws.sizes = (int(batch), h, _grid_tuple(grid), int(block))
     ws.params = [tuple(int(x) for x in m) for m in params]
     return (ws, kept) if return_kept_per_row else ws
@@ -195,9 +204,6 @@ def run(q, k, v, grid, block, workspace, scale=None, out=None, return_lse=False,
     _check_qkv(q, k, v)
     b, h, n, d = q.shape
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    o = torch.empty_like(q) if out is None else out
-    _check_qkv(q, o)
-    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
     _check_tokens(n, grid)
     ws = workspace
     if ws.params is None:
@@ -205,10 +211,13 @@ def run(q, k, v, grid, block, workspace, scale=None, out=None, return_lse=False,
     if ws.sizes != (b, h, _grid_tuple(grid), int(block)):
         raise ValueError("the workspace was planned for (batch, heads, grid, block) = %s, not %s"
                          % (ws.sizes, (b, h, _grid_tuple(grid), int(block))))
-    with torch.cuda.device(q.device):
+    with torch.cuda.device(q.device), _on(stream):
+        o = torch.empty_like(q) if out is None else out
+        _check_qkv(q, o)
+        lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
         _lib.check(_lib.lib().psa_attention_run(
             _ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, _grid(grid), int(block), scale,
-            _ptr(ws.tensor), ws.nbytes, _ptr(lse), _stream(stream, q.device)))
+            _ptr(ws.tensor), ws.nbytes, _ptr(lse), _stream(None, q.device)))
     return (o, lse) if return_lse else o
 
 
@@ -228,22 +237,18 @@ def dense_fwd(q, k, v, block, scale=None, out=None, return_lse=False, stream=Non
     _check_qkv(q, k, v)
     b, h, n, d = q.shape
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    o = torch.empty_like(q) if out is None else out
-    _check_qkv(q, o)
-    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
-    if not balanced:
-        workspace = None
-    elif workspace is None:
-        # Allocated on the current stream; a call on another stream keeps it alive until that
-        # stream has consumed it.
-        workspace = torch.empty(dense_workspace_size(), dtype=torch.uint8, device=q.device)
-        if stream is not None:
-            workspace.record_stream(stream)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    with torch.cuda.device(q.device):
+    with torch.cuda.device(q.device), _on(stream):
+        o = torch.empty_like(q) if out is None else out
+        _check_qkv(q, o)
+        lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
+        if not balanced:
+            workspace = None
+        elif workspace is None:
+            workspace = torch.empty(dense_workspace_size(), dtype=torch.uint8, device=q.device)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         _lib.check(_lib.lib().psa_dense_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, n, int(block),
                                             scale, _ptr(lse), _ptr(workspace), ws_bytes,
-                                            _stream(stream, q.device)))
+                                            _stream(None, q.device)))
     return (o, lse) if return_lse else o
 
 
@@ -270,13 +275,13 @@ def _layout(src, grid, pb, out, stream, to):
         raise ValueError("tensor has %d tokens, the %s layout has %d" % (n, "original" if to else "blocked",
                                                                         n_orig if to else n_blk))
     shape = (b, h, n_blk if to else n_orig, d)
-    dst = torch.empty(shape, dtype=src.dtype, device=src.device) if out is None else out
-    if tuple(dst.shape) != shape or not dst.is_contiguous() or dst.dtype != src.dtype:
-        raise ValueError("out must be a contiguous bf16 tensor of shape %s" % (shape,))
     fn = _lib.lib().psa_to_blocks if to else _lib.lib().psa_from_blocks
-    with torch.cuda.device(src.device):
+    with torch.cuda.device(src.device), _on(stream):
+        dst = torch.empty(shape, dtype=src.dtype, device=src.device) if out is None else out
+        if tuple(dst.shape) != shape or not dst.is_contiguous() or dst.dtype != src.dtype:
+            raise ValueError("out must be a contiguous bf16 tensor of shape %s" % (shape,))
         _lib.check(fn(_ptr(src), _ptr(dst), b * h, d, _grid(grid), _lib.block3d_of(pb),
-                      _stream(stream, src.device)))
+                      _stream(None, src.device)))
     return dst
 
 
@@ -300,13 +305,13 @@ def build_blockmap_3d(params, grid, pb, device=None, blockmap=True, per_row=True
     (tp, hp, wp) = (-(-g[0] // pb[0]), -(-g[1] // pb[1]), -(-g[2] // pb[2]))
     groups = tp * hp * wp + (1 if g[3] > 0 else 0)
     heads = len(params)
-    bm = torch.empty((heads, groups, groups), dtype=torch.uint8, device=device) if blockmap else None
-    pr = torch.empty((heads, groups), dtype=torch.int32, device=device) if per_row else None
-    ph = torch.empty((heads,), dtype=torch.int64, device=device) if per_head else None
-    with torch.cuda.device(device):
+    with torch.cuda.device(device), _on(stream):
+        bm = torch.empty((heads, groups, groups), dtype=torch.uint8, device=device) if blockmap else None
+        pr = torch.empty((heads, groups), dtype=torch.int32, device=device) if per_row else None
+        ph = torch.empty((heads,), dtype=torch.int64, device=device) if per_head else None
         _lib.check(_lib.lib().psa_build_blockmap_3d(_lib.stripes(params), heads, _grid(grid),
                                                     _lib.block3d_of(pb), _ptr(bm), _ptr(pr), _ptr(ph),
-                                                    _stream(stream, device)))
+                                                    _stream(None, device)))
     return bm, pr, ph
 
 
@@ -330,13 +335,13 @@ def plan_3d(params, grid, pb, tile=128, batch=1, device=None, workspace=None,
     torch = _torch()
     device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
     h = len(params)
-    ws = workspace if workspace is not None else Workspace3d(batch, h, grid, pb, tile, device)
     n_tiles = -(-blocked_tokens(grid, pb) // int(tile))
-    kept = torch.empty((h, n_tiles), dtype=torch.int32, device=device) if return_kept_per_tile else None
-    with torch.cuda.device(device):
+    with torch.cuda.device(device), _on(stream):
+        ws = workspace if workspace is not None else Workspace3d(batch, h, grid, pb, tile, device)
+        kept = torch.empty((h, n_tiles), dtype=torch.int32, device=device) if return_kept_per_tile else None
         _lib.check(_lib.lib().psa_attention_plan_3d(int(batch), h, _grid(grid), _lib.block3d_of(pb),
                                                     int(tile), _lib.stripes(params), _ptr(ws.tensor),
-                                                    ws.nbytes, _ptr(kept), _stream(stream, device)))
+                                                    ws.nbytes, _ptr(kept), _stream(None, device)))
     ws.sizes = (int(batch), h, _grid_tuple(grid), tuple(int(x) for x in pb), int(tile))
     ws.params = [tuple(int(x) for x in m) for m in params]
     return (ws, kept) if return_kept_per_tile else ws
@@ -350,19 +355,19 @@ def run_3d(q, k, v, grid, pb, tile, workspace, scale=None, out=None, return_lse=
     if n != blocked_tokens(grid, pb):
         raise ValueError("q, k, v must be in the PSABlock-centric layout (%d tokens)" % blocked_tokens(grid, pb))
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    o = torch.empty_like(q) if out is None else out
-    _check_qkv(q, o)
-    lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
     ws = workspace
     if ws.params is None:
         raise ValueError("the workspace holds no plan: call plan_3d() first")
     if ws.sizes != (b, h, _grid_tuple(grid), tuple(int(x) for x in pb), int(tile)):
         raise ValueError("the workspace was planned for %s, not %s"
                          % (ws.sizes, (b, h, _grid_tuple(grid), tuple(pb), int(tile))))
-    with torch.cuda.device(q.device):
+    with torch.cuda.device(q.device), _on(stream):
+        o = torch.empty_like(q) if out is None else out
+        _check_qkv(q, o)
+        lse = torch.empty((b, h, n), dtype=torch.float32, device=q.device) if return_lse else None
         _lib.check(_lib.lib().psa_attention_run_3d(
             _ptr(q), _ptr(k), _ptr(v), _ptr(o), b, h, d, _grid(grid), _lib.block3d_of(pb), int(tile),
-            scale, _ptr(ws.tensor), ws.nbytes, _ptr(lse), _stream(stream, q.device)))
+            scale, _ptr(ws.tensor), ws.nbytes, _ptr(lse), _stream(None, q.device)))
     return (o, lse) if return_lse else o
 
 
@@ -383,16 +388,16 @@ def l2_distance(o, ref, sq_err=None, sq_ref=None, workspace=None, stream=None):
     torch = _torch()
     _check_qkv(o, ref)
     b, h, n, d = o.shape
-    err = torch.empty((b, h), dtype=torch.float64, device=o.device) if sq_err is None else sq_err
-    rref = torch.empty((b, h), dtype=torch.float64, device=o.device) if sq_ref is None else sq_ref
-    for t in (err, rref):
-        if t.dtype != torch.float64 or t.numel() != b * h or not t.is_contiguous():
-            raise ValueError("sq_err and sq_ref must be contiguous float64 tensors of %d elements" % (b * h))
     nbytes = int(_lib.lib().psa_l2_workspace_size(b * h))
-    ws = torch.empty(nbytes, dtype=torch.uint8, device=o.device) if workspace is None else workspace
-    if ws.numel() < nbytes:
-        raise ValueError("l2 workspace needs %d bytes" % nbytes)
-    with torch.cuda.device(o.device):
+    with torch.cuda.device(o.device), _on(stream):
+        err = torch.empty((b, h), dtype=torch.float64, device=o.device) if sq_err is None else sq_err
+        rref = torch.empty((b, h), dtype=torch.float64, device=o.device) if sq_ref is None else sq_ref
+        for t in (err, rref):
+            if t.dtype != torch.float64 or t.numel() != b * h or not t.is_contiguous():
+                raise ValueError("sq_err and sq_ref must be contiguous float64 tensors of %d elements" % (b * h))
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=o.device) if workspace is None else workspace
+        if ws.numel() < nbytes:
+            raise ValueError("l2 workspace needs %d bytes" % nbytes)
         _lib.check(_lib.lib().psa_l2_distance(_ptr(o), _ptr(ref), b * h, n, d, _ptr(err), _ptr(rref),
-                                              _ptr(ws), ws.numel(), _stream(stream, o.device)))
+                                              _ptr(ws), ws.numel(), _stream(None, o.device)))
     return err, rref

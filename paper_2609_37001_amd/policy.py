@@ -7,7 +7,7 @@ runs the dense kernel during the exempt steps and the planned sparse kernel afte
 """
 import math
 
-from . import Workspace, dense_fwd, plan, run
+from . import dense_fwd, plan, run
 
 
 class TimestepPolicy:
@@ -37,15 +37,16 @@ class LayerAttention:
         self.workspace = None
         self.device = device
 
-    def _planned(self, device):
+    def _planned(self, device, stream):
+        # The plan is enqueued on the stream of the run that first needs it, so the run follows
+        # it; a later run on another stream is ordered by the caller, as for any input.
         if self.workspace is None:
-            ws = Workspace(self.batch, len(self.params), self.grid, self.block, device)
             self.workspace = plan(self.params, self.grid, self.block, batch=self.batch, device=device,
-                                  workspace=ws)
+                                  stream=stream)
         return self.workspace
 
     def __call__(self, q, k, v, step, out=None, stream=None):
         if self.policy.is_dense(step):
             return dense_fwd(q, k, v, self.block, self.scale, out=out, stream=stream)
-        return run(q, k, v, self.grid, self.block, self._planned(q.device), self.scale, out=out,
-                   stream=stream)
+        return run(q, k, v, self.grid, self.block, self._planned(q.device, stream), self.scale,
+                   out=out, stream=stream)

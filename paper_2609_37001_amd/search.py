@@ -30,31 +30,37 @@ class HeadResults:
 
 
 def score(q, k, v, grid, block, candidates, scale=None, stream=None):
-    """HeadResults of candidates[h][c] for q, k, v bf16 [batch, heads, N, d] on the GPU."""
+    """HeadResults of candidates[h][c] for q, k, v bf16 [batch, heads, N, d] on the GPU.
+
+    With a stream given, every step runs on it (allocations, library calls and the reductions
+    whose results are read on the host); the caller orders q, k, v onto it."""
+    import contextlib
     import torch
     b, h, n, d = q.shape
     n_cand = len(candidates[0])
     if len(candidates) != h or any(len(c) != n_cand for c in candidates):
         raise ValueError("candidates must list the same number of masks for every head")
-    full = dense_fwd(q, k, v, block, scale, stream=stream)
-    o = torch.empty_like(q)
-    ws = Workspace(b, h, grid, block, q.device)
-    sq_err = torch.empty((n_cand, b, h), dtype=torch.float64, device=q.device)
-    sq_ref = torch.empty((b, h), dtype=torch.float64, device=q.device)
-    l2_ws = torch.empty(int(_lib.lib().psa_l2_workspace_size(b * h)), dtype=torch.uint8, device=q.device)
-    kept = torch.empty((n_cand, h), dtype=torch.int64, device=q.device)
-    for c in range(n_cand):
-        params = [candidates[hh][c] for hh in range(h)]
-        # the plan's per-row kept counts give the sparsity without another pass over the map
-        _, per_row = attention_fwd(q, k, v, grid, block, params, scale, out=o, workspace=ws,
-                                   return_kept_per_row=True, stream=stream)
-        l2_distance(o, full, sq_err=sq_err[c], sq_ref=sq_ref, workspace=l2_ws, stream=stream)
-        kept[c] = per_row.sum(dim=1)
-    err = sq_err.sum(dim=1).cpu().numpy()                 # [C, heads]: over batch elements
-    ref = sq_ref.sum(dim=0).cpu().numpy()                 # [heads]
+    with (contextlib.nullcontext() if stream is None else torch.cuda.stream(stream)):
+        full = dense_fwd(q, k, v, block, scale)
+        o = torch.empty_like(q)
+        ws = Workspace(b, h, grid, block, q.device)
+        sq_err = torch.empty((n_cand, b, h), dtype=torch.float64, device=q.device)
+        sq_ref = torch.empty((b, h), dtype=torch.float64, device=q.device)
+        l2_ws = torch.empty(int(_lib.lib().psa_l2_workspace_size(b * h)), dtype=torch.uint8, device=q.device)
+        kept = torch.empty((n_cand, h), dtype=torch.int64, device=q.device)
+        for c in range(n_cand):
+            params = [candidates[hh][c] for hh in range(h)]
+            # the plan's per-row kept counts give the sparsity without another pass over the map
+            _, per_row = attention_fwd(q, k, v, grid, block, params, scale, out=o, workspace=ws,
+                                       return_kept_per_row=True)
+            l2_distance(o, full, sq_err=sq_err[c], sq_ref=sq_ref, workspace=l2_ws)
+            kept[c] = per_row.sum(dim=1)
+        err = sq_err.sum(dim=1).cpu().numpy()             # [C, heads]: over batch elements
+        ref = sq_ref.sum(dim=0).cpu().numpy()             # [heads]
+        kept_n = kept.cpu().numpy()
     nb = -(-n // block)
     loss = np.sqrt(err / np.where(ref > 0, ref, 1.0)).T   # [heads, C]
-    sparsity = 1.0 - kept.cpu().numpy().T.astype(np.float64) / float(nb * nb)
+    sparsity = 1.0 - kept_n.T.astype(np.float64) / float(nb * nb)
     return HeadResults([list(c) for c in candidates], loss, sparsity)
 
 

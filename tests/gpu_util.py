@@ -1,4 +1,4 @@
-"""Helpers shared by the GPU parity tests: device inputs, sampled oracle comparison, metrics."""
+"""Helpers shared by the GPU parity tests: device inputs, oracle comparison, metrics."""
 import functools
 import math
 
@@ -8,13 +8,28 @@ import oracle
 from workloads import get_config, make_head_qkv, make_qkv, stripe_params
 from workloads.inputs import bf16_round, rope_tables
 
-REL_L2_TOL = 1e-2      # relative L2 error of O against the oracle
+REL_L2_TOL = 1e-2      # relative L2 error of O against the oracle, pooled over the compared rows
 MAX_ABS_TOL = 3e-2     # max absolute error of O against the oracle
+# Every single query row's relative L2 error, and the largest element error relative to the
+# largest output element of the compared rows.  Outputs are averages over hundreds to tens of
+# thousands of keys at the workload sizes (|O| ~ 0.005-0.05), so the absolute bound above cannot
+# see an error confined to a few rows; these two can.  The errors come from three roundings of
+# relative size 2^-9 each (the scaled q, P and O to bf16): about 3e-3 pooled, at most 4.2e-3 for a
+# row of the workloads.  A row that keeps few keys averages few, partly cancelling values, so P's
+# rounding does not average out there: up to 1.0e-2 in the small random cases (|O| up to 3.8).
+# Hence twice the benchmark spec's relative L2 bound per row; a dropped or misplaced key block moves
+# its rows by far more (and the structured full-size test checks that part exactly).
+ROW_REL_TOL = 2e-2
+PEAK_REL_TOL = 1e-2
 # Absolute error of the natural-log normaliser against the oracle evaluated on the kernel's own
 # operand (kernel_q): the kernel sums the bf16-rounded weights into l.  bf16 keeps 8 significant
 # bits, so each weight, and hence the sum, is off by a relative 2^-8 at most:
 # ln(1 + 2^-8) = 3.9e-3; 4e-3 with fp32 accumulation and the exp2/log2 approximations.
 LSE_ABS_TOL = 4e-3
+# Largest relative change of an element of q in the kernel's operand bf16(q * fl32(scale log2 e)):
+# 2^-9 for the bf16 rounding (round to nearest even), plus 2^-24 for the fp32 product and about
+# 2^-23 for the fp32 constant; 1.01 covers both.
+Q_ROUND = 2.0 ** -9 * 1.01
 LN2 = math.log(2.0)
 
 
@@ -24,6 +39,100 @@ def kernel_q(q, scale):
     ln 2 evaluated on it is the kernel's exp2-domain softmax of exactly these inputs."""
     c = np.float32(scale) * np.float32(1.4426950408889634)
     return bf16_round(np.asarray(q, dtype=np.float32) * c)
+
+
+def lse_plain_bound(q, k, rows, scale):
+    """Per-row bound of |LSE_kernel - LSE(q as given)|.  The kernel's scores are those of
+    kernel_q(q), in which each element of q moves by a relative Q_ROUND at most, so score j of
+    row i moves by at most Q_ROUND * scale * sum_c |q_ic k_jc|.  The log-sum-exp of a score vector
+    moves by at most the largest move of a score (its gradient is a probability vector, so the
+    mean value theorem bounds the change by the largest entry of the move); the largest over all
+    keys bounds the largest over the kept ones.  LSE_ABS_TOL adds the kernel's own arithmetic on
+    that operand."""
+    qa = np.abs(np.asarray(q, dtype=np.float64))
+    qa = qa if rows is None else qa[np.asarray(rows)]
+    a = qa @ np.abs(np.asarray(k, dtype=np.float64)).T
+    return LSE_ABS_TOL + Q_ROUND * scale * a.max(axis=1)
+
+
+class Parity:
+    """Error statistics of device rows against oracle rows, and the parity bar's asserts."""
+
+    def __init__(self):
+        self.num = self.den = 0.0
+        self.max_abs = self.max_ref = self.max_row = 0.0
+        self.max_lse = 0.0           # against the oracle on the kernel's operand
+        self.max_lse_plain = 0.0     # against the oracle on the inputs as given
+        self.lse_plain_ratio = 0.0   # largest (error / per-row bound) on the inputs as given
+        self.rows = 0
+
+    def add(self, o, o_ref, lse=None, lse_kernel_ref=None, lse_ref=None, lse_bound=None):
+        o = np.asarray(o, dtype=np.float64)
+        o_ref = np.asarray(o_ref, dtype=np.float64)
+        d = o - o_ref
+        self.num += float((d ** 2).sum())
+        self.den += float((o_ref ** 2).sum())
+        self.max_abs = max(self.max_abs, float(np.abs(d).max()))
+        self.max_ref = max(self.max_ref, float(np.abs(o_ref).max()))
+        row_err = np.sqrt((d ** 2).sum(axis=1))
+        row_ref = np.sqrt((o_ref ** 2).sum(axis=1))
+        live = row_ref > 0
+        assert (row_err[~live] == 0).all(), "rows with no kept key must give o = 0"
+        if live.any():
+            self.max_row = max(self.max_row, float((row_err[live] / row_ref[live]).max()))
+        if lse is not None:
+            lse = np.asarray(lse, dtype=np.float64)
+            fin = np.isfinite(lse_kernel_ref)
+            assert (np.isneginf(lse) == ~fin).all(), "rows with no kept key must give lse = -inf"
+            assert (np.isfinite(lse_ref) == fin).all()
+            if fin.any():
+                self.max_lse = max(self.max_lse, float(np.abs(lse[fin] - lse_kernel_ref[fin]).max()))
+                e = np.abs(lse[fin] - lse_ref[fin])
+                self.max_lse_plain = max(self.max_lse_plain, float(e.max()))
+                self.lse_plain_ratio = max(self.lse_plain_ratio, float((e / lse_bound[fin]).max()))
+        self.rows += o.shape[0]
+
+    @property
+    def rel(self):
+        return math.sqrt(self.num / self.den) if self.den > 0 else (0.0 if self.num == 0 else math.inf)
+
+    def summary(self):
+        return ("%d rows: rel_l2 %.2e, worst row %.2e, max_abs %.2e (%.2e of max|O| %.2e), lse %.2e, "
+                "lse vs plain inputs %.2e (%.2f of its bound)"
+                % (self.rows, self.rel, self.max_row, self.max_abs,
+                   self.max_abs / self.max_ref if self.max_ref > 0 else 0.0, self.max_ref,
+                   self.max_lse, self.max_lse_plain, self.lse_plain_ratio))
+
+    def check(self, label=""):
+        print("%s %s" % (label, self.summary()))
+        assert self.rel <= REL_L2_TOL, self.summary()
+        assert self.max_abs <= MAX_ABS_TOL, self.summary()
+        assert self.max_row <= ROW_REL_TOL, self.summary()
+        assert self.max_abs <= PEAK_REL_TOL * self.max_ref or self.max_abs == 0, self.summary()
+        assert self.max_lse <= LSE_ABS_TOL, self.summary()
+        assert self.lse_plain_ratio <= 1.0, self.summary()
+
+
+def compare_head(par, q, k, v, keep, block, scale, o, lse=None, rows=None, groups=None):
+    """Adds the device rows of one (batch, head) -- o [R, d], lse [R] or None, for query rows
+    `rows` (all if None) -- and the oracle's rows of the same inputs to `par`."""
+    o_ref, lse_ref = oracle.masked_attention(q, k, v, keep, block, scale, rows, groups=groups)
+    lse_k = bound = None
+    if lse is not None:
+        _, lse_k = oracle.masked_attention(kernel_q(q, scale), k, v, keep, block, LN2, rows, groups=groups)
+        bound = lse_plain_bound(q, k, rows, scale)
+    par.add(o, o_ref, lse, lse_k, lse_ref, bound)
+
+
+def compare_all(q, k, v, keep, block, scale, o, lse, groups=None, rows=None):
+    """Every (batch, head) of numpy [B, H, N, d] inputs against device results (numpy o [B, H, N, d]
+    or [B, H, R, d], lse [B, H, N] or [B, H, R]); returns the Parity."""
+    par = Parity()
+    for bi in range(q.shape[0]):
+        for hi in range(q.shape[1]):
+            compare_head(par, q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale, o[bi, hi],
+                         None if lse is None else lse[bi, hi], rows=rows, groups=groups)
+    return par
 
 
 def torch():
@@ -76,12 +185,10 @@ def sample_blocks(cfg, bmap, n_random=6, seed=0):
 
 
 def compare_rows(cfg, params, bmap, o_dev, lse_dev, picks, batch=0):
-    """Oracle rows of the sampled (head, query block) pairs against the device output.
-
-    Returns (rel_l2, max_abs, max_abs_lse) pooled over every sampled row."""
+    """Oracle rows of the sampled (head, query block) pairs against the device output; returns
+    the Parity of every sampled row."""
     tables = rope_tables(cfg)
-    num = den = 0.0
-    max_abs = max_lse = 0.0
+    par = Parity()
     by_head = {}
     for h, qb in picks:
         by_head.setdefault(h, []).append(qb)
@@ -89,22 +196,10 @@ def compare_rows(cfg, params, bmap, o_dev, lse_dev, picks, batch=0):
         q, k, v = make_head_qkv(cfg, batch, h, tables)
         rows = np.concatenate([np.arange(qb * cfg.block, min(cfg.n_tokens, (qb + 1) * cfg.block))
                                for qb in qbs])
-        o_ref, _ = oracle.masked_attention(q, k, v, bmap[h], cfg.block, cfg.scale, rows)
-        o = o_dev[batch, h, rows].float().cpu().numpy().astype(np.float64)
-        num += float(((o - o_ref) ** 2).sum())
-        den += float((o_ref ** 2).sum())
-        max_abs = max(max_abs, float(np.abs(o - o_ref).max()))
-        if lse_dev is not None:
-            _, lse_ref = oracle.masked_attention(kernel_q(q, cfg.scale), k, v, bmap[h], cfg.block,
-                                                 LN2, rows)
-            lse = lse_dev[batch, h, rows].cpu().numpy().astype(np.float64)
-            fin = np.isfinite(lse_ref)
-            assert (np.isneginf(lse) == ~fin).all(), "empty rows must give lse = -inf"
-            if fin.any():
-                max_lse = max(max_lse, float(np.abs(lse[fin] - lse_ref[fin]).max()))
-            assert (o[~fin] == 0).all(), "empty rows must give o = 0"
-    rel = (num / den) ** 0.5 if den > 0 else (0.0 if num == 0 else float("inf"))
-    return rel, max_abs, max_lse
+        o = o_dev[batch, h, rows].float().cpu().numpy()
+        lse = None if lse_dev is None else lse_dev[batch, h, rows].cpu().numpy()
+        compare_head(par, q, k, v, bmap[h], cfg.block, cfg.scale, o, lse, rows=rows)
+    return par
 
 
 def params_of(name, target=None):

@@ -1,6 +1,4 @@
 """GPU attention parity against the oracle (sampled rows at full size, full tensors when small)."""
-import math
-
 import numpy as np
 import pytest
 
@@ -21,26 +19,8 @@ def dev(x):
 
 
 def full_compare(q, k, v, keep, block, scale, o, lse):
-    """Every row of a [B, H, N, d] problem against the oracle (O on the inputs as given, LSE on
-    the kernel's rounded operand, see gpu_util.kernel_q)."""
-    b, h, n, d = q.shape
-    num = den = mx = mlse = 0.0
-    for bi in range(b):
-        for hi in range(h):
-            o_ref, _ = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale)
-            _, l_ref = oracle.masked_attention(gu.kernel_q(q[bi, hi], scale), k[bi, hi], v[bi, hi],
-                                               keep[hi], block, gu.LN2)
-            og = o[bi, hi].float().cpu().numpy().astype(np.float64)
-            num += ((og - o_ref) ** 2).sum()
-            den += (o_ref ** 2).sum()
-            mx = max(mx, np.abs(og - o_ref).max())
-            lg = lse[bi, hi].cpu().numpy().astype(np.float64)
-            fin = np.isfinite(l_ref)
-            assert (np.isneginf(lg) == ~fin).all()
-            assert (og[~fin] == 0).all()
-            if fin.any():
-                mlse = max(mlse, np.abs(lg[fin] - l_ref[fin]).max())
-    return math.sqrt(num / den), mx, mlse
+    """Every row of a [B, H, N, d] problem against the oracle (gpu_util.Parity)."""
+    return gu.compare_all(q, k, v, keep, block, scale, o.float().cpu().numpy(), lse.cpu().numpy())
 
 
 def random_problem(b, h, n, d, seed):
@@ -58,9 +38,7 @@ def test_tiny_config_full():
     bmap = gu.oracle_map(cfg, params)
     assert (kept.cpu().numpy() == oracle.kept_per_row(bmap)).all()
     qn, kn, vn = (x.float().cpu().numpy() for x in (q, k, v))
-    rel, mx, mlse = full_compare(qn, kn, vn, bmap, cfg.block, cfg.scale, o, lse)
-    print("tiny: rel_l2 %.2e max_abs %.2e lse %.2e" % (rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    full_compare(qn, kn, vn, bmap, cfg.block, cfg.scale, o, lse).check("tiny:")
 
 
 @pytest.mark.parametrize("d,block", [(64, 64), (128, 128), (128, 64), (64, 128)])
@@ -75,9 +53,7 @@ def test_shapes_ragged_text_batch(d, block):
     keep = oracle.blockmap(params, f, hh, ww, nt, block)
     o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, nt), block, params, 0.11, return_lse=True)
     gu.torch().cuda.synchronize()
-    rel, mx, mlse = full_compare(q, k, v, keep, block, 0.11, o, lse)
-    print("d=%d block=%d: rel_l2 %.2e max_abs %.2e lse %.2e" % (d, block, rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    full_compare(q, k, v, keep, block, 0.11, o, lse).check("d=%d block=%d:" % (d, block))
 
 
 def test_long_text_rows_scheduled_first():
@@ -93,9 +69,7 @@ def test_long_text_rows_scheduled_first():
     assert (rows[:, -3:] * rows.size > 3 * rows.sum()).all() and (rows[:, :-3] * rows.size <= 3 * rows.sum()).all()
     o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, nt), 128, params, 0.1, return_lse=True)
     gu.torch().cuda.synchronize()
-    rel, mx, mlse = full_compare(q, k, v, keep, 128, 0.1, o, lse)
-    print("long text rows: rel_l2 %.2e max_abs %.2e lse %.2e" % (rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    full_compare(q, k, v, keep, 128, 0.1, o, lse).check("long text rows:")
 
 
 @pytest.mark.parametrize("d,block", [(64, 64), (128, 128)])
@@ -106,9 +80,7 @@ def test_dense_full(d, block):
     keep = np.ones((3, nb, nb), np.uint8)
     o, lse = psa.dense_fwd(dev(q), dev(k), dev(v), block, 0.09, return_lse=True)
     gu.torch().cuda.synchronize()
-    rel, mx, mlse = full_compare(q, k, v, keep, block, 0.09, o, lse)
-    print("dense d=%d: rel_l2 %.2e max_abs %.2e lse %.2e" % (d, rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    full_compare(q, k, v, keep, block, 0.09, o, lse).check("dense d=%d:" % d)
 
 
 @pytest.mark.parametrize("d,block", [(64, 64), (128, 128), (128, 64), (64, 128)])
@@ -217,19 +189,32 @@ def test_run_without_matching_plan_writes_nothing():
 
 
 def test_layer_attention_follows_the_timestep_policy():
-    """Dense kernel during the exempt steps, the layer's single plan afterwards (same bits as the
-    direct calls)."""
+    """Sec. 4 setup: the first 20 % of the denoising steps stay dense.  Over 10 steps the exempt
+    steps 0-1 give full attention and steps 2-9 the layer's stripes, each against the oracle (full
+    map, and the masked attention of the stripes' map); the layer plans once, and its outputs carry
+    the bits of the direct dense and sparse calls."""
     from paper_2609_37001_amd.policy import LayerAttention, TimestepPolicy
     torch = gu.torch()
-    f, hh, ww = 3, 8, 16
+    f, hh, ww, nt = 4, 16, 24, 40
+    grid = (f, hh, ww, nt)
+    n = f * hh * ww + nt
     params = [(1, 0, INF, 2, 0, INF), (2, 1, 3, 1, 0, INF)]
-    q, k, v = (dev(x) for x in random_problem(1, 2, f * hh * ww, 128, seed=21))
-    layer = LayerAttention(params, (f, hh, ww), 128, 1, TimestepPolicy(10, 0.2), scale=0.1)
-    dense = psa.dense_fwd(q, k, v, 128, 0.1)
-    sparse = psa.attention_fwd(q, k, v, (f, hh, ww), 128, params, 0.1)
+    qn, kn, vn = random_problem(1, 2, n, 128, seed=21)
+    q, k, v = dev(qn), dev(kn), dev(vn)
+    layer = LayerAttention(params, grid, 128, 1, TimestepPolicy(10, 0.2), scale=0.1)
+    assert [layer.policy.is_dense(s) for s in range(10)] == [True] * 2 + [False] * 8
     outs = [layer(q, k, v, step) for step in range(10)]
+    dense = psa.dense_fwd(q, k, v, 128, 0.1)
+    sparse = psa.attention_fwd(q, k, v, grid, 128, params, 0.1)
     torch.cuda.synchronize()
     ws = layer.workspace
     assert all(torch.equal(o, dense) for o in outs[:2])
     assert all(torch.equal(o, sparse) for o in outs[2:])
     assert layer.workspace is ws
+    nb = -(-n // 128)
+    full = np.ones((2, nb, nb), dtype=np.uint8)
+    keep = oracle.blockmap(params, f, hh, ww, nt, 128)
+    assert not keep.all()
+    on = lambda o: o.float().cpu().numpy()
+    gu.compare_all(qn, kn, vn, full, 128, 0.1, on(outs[0]), None).check("exempt step 0 vs full attention:")
+    gu.compare_all(qn, kn, vn, keep, 128, 0.1, on(outs[5]), None).check("step 5 vs the stripes' map:")

@@ -20,24 +20,11 @@ def dev(x):
     return t.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to("cuda:0").bfloat16()
 
 
-def check(q, k, v, keep, block, scale, o, lse, rows=None):
-    num = den = 0.0
-    for bi in range(q.shape[0]):
-        for hi in range(q.shape[1]):
-            o_ref, _ = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale, rows)
-            _, l_ref = oracle.masked_attention(gu.kernel_q(q[bi, hi], scale), k[bi, hi], v[bi, hi], keep[hi],
-                                               block, gu.LN2, rows)
-            r = slice(None) if rows is None else rows
-            og, lg = o[bi, hi][r].astype(np.float64), lse[bi, hi][r].astype(np.float64)
-            fin = np.isfinite(l_ref)
-            assert (np.isneginf(lg) == ~fin).all() and (og[~fin] == 0).all()
-            if fin.any():
-                assert np.abs(lg[fin] - l_ref[fin]).max() <= gu.LSE_ABS_TOL
-                assert np.abs(og - o_ref).max() <= gu.MAX_ABS_TOL
-            num += ((og - o_ref) ** 2).sum()
-            den += (o_ref ** 2).sum()
-    if den > 0:
-        assert (num / den) ** 0.5 <= gu.REL_L2_TOL
+def check(q, k, v, keep, block, scale, o, lse, rows=None, label=""):
+    """Rows `rows` (all if None) of every (batch, head) against the oracle (gpu_util.Parity)."""
+    if rows is not None:
+        o, lse = o[:, :, rows], lse[:, :, rows]
+    gu.compare_all(q, k, v, keep, block, scale, o, lse, rows=rows).check(label)
 
 
 @pytest.mark.parametrize("d,block", [(64, 64), (128, 128)])
@@ -64,9 +51,13 @@ def test_largest_block_count():
     rng = np.random.default_rng(5)
     q, k, v = (bf16_round(rng.standard_normal((1, 2, n, 128)).astype(np.float32)) for _ in range(3))
     params = [(1, 0, INF, 2, 0, INF), (3, 1, INF, 1, 0, 3)]      # own frame / three frames, nearby slots
-    o, lse, kept = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww), block, params, 0.09,
+    torch = gu.torch()
+    qd = dev(q)
+    o = torch.full_like(qd, float("nan"))                         # a row never written stays NaN
+    o, lse, kept = psa.attention_fwd(qd, dev(k), dev(v), (f, hh, ww), block, params, 0.09, out=o,
                                      return_lse=True, return_kept_per_row=True)
-    gu.torch().cuda.synchronize()
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
     keep = oracle.blockmap(params, f, hh, ww, 0, block)
     assert np.array_equal(kept.cpu().numpy(), oracle.kept_per_row(keep))
     rows = np.concatenate([np.arange(0, 8), np.arange(n // 2, n // 2 + 8), np.arange(n - 8, n)])
@@ -86,8 +77,12 @@ def test_largest_batch_heads(block, d):
     params = [(int(rng.integers(1, 3)), int(rng.choice([0, 1, -1])), int(rng.choice([1, 2, INF])),
                int(rng.integers(1, 3)), int(rng.choice([0, 1])), int(rng.choice([1, 3, INF]))) for _ in range(h)]
     q, k, v = (bf16_round(rng.standard_normal((b, h, n, d)).astype(np.float32)) for _ in range(3))
-    o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), grid, block, params, 0.1, return_lse=True)
-    gu.torch().cuda.synchronize()
+    torch = gu.torch()
+    qd = dev(q)
+    o = torch.full_like(qd, float("nan"))
+    o, lse = psa.attention_fwd(qd, dev(k), dev(v), grid, block, params, 0.1, out=o, return_lse=True)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(o).all())
     keep = oracle.blockmap(params, *grid, block)
     check(q, k, v, keep, block, 0.1, o.float().cpu().numpy(), lse.cpu().numpy())
 

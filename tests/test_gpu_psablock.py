@@ -93,28 +93,11 @@ def test_plan_counts_per_tile(grid, pb, tile):
 
 
 def compare_3d(q, k, v, grid, pb, params, scale, o, lse):
-    """O against the oracle in the original order; LSE against the oracle on the kernel's
-    rounded operand (gpu_util.kernel_q)."""
+    """O and LSE in the original order against the oracle (gpu_util.Parity)."""
     f, h, w, nt = grid
     keep = oracle.psablock_map(params, f, h, w, nt, pb)
     groups = oracle.token_groups(f, h, w, nt, pb)
-    num = den = mx = mlse = 0.0
-    b, hh = q.shape[:2]
-    for bi in range(b):
-        for hi in range(hh):
-            o_ref, _ = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], 1, scale, groups=groups)
-            _, l_ref = oracle.masked_attention(gu.kernel_q(q[bi, hi], scale), k[bi, hi], v[bi, hi], keep[hi], 1,
-                                               gu.LN2, groups=groups)
-            og = o[bi, hi].astype(np.float64)
-            lg = lse[bi, hi].astype(np.float64)
-            num += ((og - o_ref) ** 2).sum()
-            den += (o_ref ** 2).sum()
-            mx = max(mx, np.abs(og - o_ref).max())
-            fin = np.isfinite(l_ref)
-            assert (np.isneginf(lg) == ~fin).all() and (og[~fin] == 0).all()
-            if fin.any():
-                mlse = max(mlse, np.abs(lg[fin] - l_ref[fin]).max())
-    return (num / den) ** 0.5, mx, mlse
+    return gu.compare_all(q, k, v, keep, 1, scale, o, lse, groups=groups)
 
 
 @pytest.mark.parametrize("d,tile,grid,pb", [
@@ -137,9 +120,8 @@ def test_attention_3d_against_oracle(d, tile, grid, pb):
     lse_b = lseb.cpu().numpy()
     lse = np.stack([np.stack([oracle.from_blocks(lse_b[bi, hi][:, None], f, h, w, nt, pb)[:, 0]
                               for hi in range(len(params))]) for bi in range(2)])
-    rel, mx, mlse = compare_3d(q, k, v, grid, pb, params, 0.11, o.float().cpu().numpy(), lse)
-    print("3d d=%d tile=%d: rel_l2 %.2e max_abs %.2e lse %.2e" % (d, tile, rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    compare_3d(q, k, v, grid, pb, params, 0.11, o.float().cpu().numpy(), lse).check(
+        "3d d=%d tile=%d:" % (d, tile))
 
 
 def test_attention_3d_plan_reuse_and_deterministic():
@@ -180,20 +162,12 @@ def test_wan14b_psablock_workload_sampled():
     picks = [(0, 44 * 80 + 3), (7, 0), (cfg.heads - 1, cfg.n_tokens - 1)]
     picks += [(int(rng.integers(cfg.heads)), int(rng.integers(cfg.n_tokens))) for _ in range(5)]
     lse_b = lseb.cpu().numpy()
-    num = den = mx = mlse = 0.0
+    par = gu.Parity()
     for h, i in picks:
         qh, kh, vh = make_head_qkv(cfg, 0, h, tables)
         rows = np.arange(max(0, i - 63), min(cfg.n_tokens, i + 65))
-        o_ref, _ = oracle.masked_attention(qh, kh, vh, keep[h], 1, cfg.scale, rows, groups=groups)
-        _, l_ref = oracle.masked_attention(gu.kernel_q(qh, cfg.scale), kh, vh, keep[h], 1, gu.LN2, rows,
-                                           groups=groups)
-        og = o[0, h, rows].float().cpu().numpy().astype(np.float64)
+        og = o[0, h, rows].float().cpu().numpy()
         lse_orig = oracle.from_blocks(lse_b[0, h][:, None], cfg.frames, cfg.height, cfg.width, cfg.n_text,
                                       cfg.psablock)[rows, 0]
-        num += ((og - o_ref) ** 2).sum()
-        den += (o_ref ** 2).sum()
-        mx = max(mx, np.abs(og - o_ref).max())
-        mlse = max(mlse, np.abs(lse_orig - l_ref).max())
-    rel = (num / den) ** 0.5
-    print("wan14b_3d: rel_l2 %.2e max_abs %.2e lse %.2e" % (rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+        gu.compare_head(par, qh, kh, vh, keep[h], 1, cfg.scale, og, lse_orig, rows=rows, groups=groups)
+    par.check("wan14b_3d:")

@@ -27,21 +27,7 @@ def random_params(rng, n, tmax, smax):
 
 
 def compare(q, k, v, keep, scale, o, lse, block=1, groups=None):
-    num = den = mx = mlse = 0.0
-    for bi in range(q.shape[0]):
-        for hi in range(q.shape[1]):
-            o_ref, _ = oracle.masked_attention(q[bi, hi], k[bi, hi], v[bi, hi], keep[hi], block, scale, groups=groups)
-            _, l_ref = oracle.masked_attention(gu.kernel_q(q[bi, hi], scale), k[bi, hi], v[bi, hi], keep[hi], block,
-                                               gu.LN2, groups=groups)
-            og, lg = o[bi, hi].astype(np.float64), lse[bi, hi].astype(np.float64)
-            num += ((og - o_ref) ** 2).sum()
-            den += (o_ref ** 2).sum()
-            mx = max(mx, np.abs(og - o_ref).max())
-            fin = np.isfinite(l_ref)
-            assert (np.isneginf(lg) == ~fin).all() and (og[~fin] == 0).all()
-            if fin.any():
-                mlse = max(mlse, np.abs(lg[fin] - l_ref[fin]).max())
-    return (num / den) ** 0.5 if den > 0 else 0.0, mx, mlse
+    return gu.compare_all(q, k, v, keep, block, scale, o, lse, groups=groups)
 
 
 @pytest.mark.parametrize("seed", range(8))
@@ -60,9 +46,8 @@ def test_random_1d(seed):
     o, lse = psa.attention_fwd(dev(q), dev(k), dev(v), (f, hh, ww, nt), block, params, scale, return_lse=True)
     gu.torch().cuda.synchronize()
     keep = oracle.blockmap(params, f, hh, ww, nt, block)
-    rel, mx, mlse = compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse.cpu().numpy(), block=block)
-    print("seed %d: n=%d d=%d block=%d rel %.2e max %.2e lse %.2e" % (seed, n, d, block, rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse.cpu().numpy(), block=block).check(
+        "seed %d: n=%d d=%d block=%d:" % (seed, n, d, block))
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -91,9 +76,8 @@ def test_random_3d(seed):
                     for h in range(heads)])[None]
     keep = oracle.psablock_map(params, f, hh, ww, nt, pb)
     groups = oracle.token_groups(f, hh, ww, nt, pb)
-    rel, mx, mlse = compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse, groups=groups)
-    print("seed %d: grid %s pb %s tile %d d %d rel %.2e max %.2e lse %.2e" % (seed, grid, pb, tile, d, rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse, groups=groups).check(
+        "seed %d: grid %s pb %s tile %d d %d:" % (seed, grid, pb, tile, d))
 
 
 def slot_major(m):
@@ -123,6 +107,5 @@ def test_random_pair_engine(seed):
     keep = oracle.blockmap(params, f, hh, ww, nt, 128)
     assert np.array_equal(kept.cpu().numpy(), oracle.kept_per_row(keep))
     assert any(slot_major(m) for m in params) and not all(slot_major(m) for m in params)
-    rel, mx, mlse = compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse.cpu().numpy(), block=128)
-    print("seed %d: n=%d nb=%d d=%d b=%d rel %.2e max %.2e lse %.2e" % (seed, n, keep.shape[1], d, b, rel, mx, mlse))
-    assert rel <= gu.REL_L2_TOL and mx <= gu.MAX_ABS_TOL and mlse <= gu.LSE_ABS_TOL
+    compare(q, k, v, keep, scale, o.float().cpu().numpy(), lse.cpu().numpy(), block=128).check(
+        "seed %d: n=%d nb=%d d=%d b=%d:" % (seed, n, keep.shape[1], d, b))
