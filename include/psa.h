@@ -35,9 +35,10 @@
  *  - Arguments are validated before anything is enqueued: on PSA_ERR_INVALID,
  *    PSA_ERR_UNSUPPORTED or PSA_ERR_WORKSPACE no output byte is written.  PSA_ERR_HIP reports a
  *    failed HIP call (launch); psa_last_error() then holds the HIP message.
- *  - The library holds no allocation and no mutable global state apart from the thread-local
- *    error message; calls are re-entrant.  Two calls that share an output or a workspace must
- *    not overlap in time.
+ *  - The library allocates nothing and holds no mutable global state apart from the thread-local
+ *    error message, the static device scratch of psa_attention_fwd_noalloc and its per-device
+ *    address table; calls are re-entrant.  Two calls that share an output, a workspace or (for
+ *    psa_attention_fwd_noalloc) a GPU's scratch must not overlap in time.
  *  - Numerics: q is multiplied by softmax_scale * log2(e) and rounded to bf16 once; bf16 x bf16
  *    products accumulated in fp32 (MFMA); softmax statistics in fp32 in the exp2 domain; P
  *    rounded to bf16 before P V, and the normaliser sums the rounded P; O rounded to bf16 (round
@@ -67,6 +68,9 @@ extern "C" {
 
 /* Largest batch * n_heads accepted by psa_attention_fwd (scheduler limit). */
 #define PSA_MAX_BATCH_HEADS 1024
+
+/* Bytes of the static device scratch of psa_attention_fwd_noalloc, per GPU (16 MiB). */
+#define PSA_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
 
 /* M(T_w, T_o, T_s, S_w, S_o, S_s) of one head (Sec. 3.2).  Widths and strides must be >= 1. */
 typedef struct {
@@ -160,6 +164,24 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
                                int32_t block, const psa_stripe_t* params, float softmax_scale,
                                void* workspace, size_t workspace_bytes, float* lse,
                                int32_t* kept_per_row, hipStream_t stream);
+
+/* psa_attention_fwd without a workspace argument and without any allocation, for callers that
+ * cannot allocate device memory: code under HIP graph capture, serving loops and harnesses that
+ * forbid hipMalloc.  The plan goes to a static device array of the library instead: every GPU the
+ * library runs on holds PSA_NOALLOC_SCRATCH_BYTES for it from the time the library's code is
+ * loaded there until the process ends.  Arguments, result and errors as psa_attention_fwd; sizes
+ * whose psa_workspace_size() exceeds PSA_NOALLOC_SCRATCH_BYTES (about 800,000 heads x blocks at
+ * batch 1; 40 heads of the Wan 2.1 14B grid take 0.5 MB) are rejected with PSA_ERR_WORKSPACE before
+ * anything is enqueued.  The call makes no allocation, free or copy: on the first call on a device
+ * it looks up the array's address on that device (hipGetSymbolAddress), then it enqueues the
+ * kernels of psa_attention_fwd.  All calls on one GPU share that GPU's array, and each leaves its
+ * plan there: calls that overlap in time on one GPU (on different streams or from different host
+ * threads) race and must not be made. */
+psa_status_t psa_attention_fwd_noalloc(const void* q, const void* k, const void* v, void* o,
+                                       int32_t batch, int32_t n_heads, int32_t head_dim,
+                                       psa_grid_t grid, int32_t block, const psa_stripe_t* params,
+                                       float softmax_scale, float* lse, int32_t* kept_per_row,
+                                       hipStream_t stream);
 
 /* Bytes of device workspace psa_dense_fwd can use (a constant: queue bounds and counters). */
 size_t psa_dense_workspace_size(void);

@@ -26,7 +26,7 @@ from . import _lib
 from ._lib import STRIDE_INF, PsaError  # noqa: F401
 
 __all__ = ["STRIDE_INF", "PsaError", "num_blocks", "workspace_size", "build_blockmap",
-           "attention_fwd", "plan", "run", "dense_fwd", "dense_workspace_size", "Workspace", "library_path",
+           "attention_fwd", "attention_fwd_noalloc", "plan", "run", "dense_fwd", "dense_workspace_size", "Workspace", "library_path",
            "blocked_tokens", "to_blocks", "from_blocks", "build_blockmap_3d", "plan_3d", "run_3d",
            "attention_fwd_3d", "l2_distance"]
 
@@ -176,6 +176,33 @@ def attention_fwd(q, k, v, grid, block, params, scale=None, out=None, return_lse
     if return_kept_per_row:
         res += (kept,)
     return res[0] if len(res) == 1 else res
+
+
+def attention_fwd_noalloc(q, k, v, grid, block, params, out, scale=None, lse=None, kept_per_row=None,
+                          stream=None):
+    """attention_fwd with the plan in the library's static device scratch
+    (psa_attention_fwd_noalloc): neither the library nor this wrapper allocates, so the caller
+    passes the output `out` (bf16 like q) and, if wanted, `lse` (float32 [batch, heads, N]) and
+    `kept_per_row` (int32 [heads, nb]).  Calls that overlap in time on one GPU must not be made."""
+    torch = _torch()
+    _check_qkv(q, k, v)
+    _check_qkv(q, out)
+    b, h, n, d = q.shape
+    if len(params) != h:
+        raise ValueError("one stripe tuple per head is required")
+    _check_tokens(n, grid)
+    nb = num_blocks(grid, block)
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (b, h, n) or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 tensor [batch, heads, N]")
+    if kept_per_row is not None and (kept_per_row.dtype != torch.int32 or tuple(kept_per_row.shape) != (h, nb)
+                                     or not kept_per_row.is_contiguous()):
+        raise ValueError("kept_per_row must be a contiguous int32 tensor [heads, nb]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    with torch.cuda.device(q.device):
+        _lib.check(_lib.lib().psa_attention_fwd_noalloc(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(out), b, h, d, _grid(grid), int(block), _lib.stripes(params),
+            scale, _ptr(lse), _ptr(kept_per_row), _stream(stream, q.device)))
+    return out
 
 
 def plan(params, grid, block, batch=1, device=None, workspace=None, return_kept_per_row=False,

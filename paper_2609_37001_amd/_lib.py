@@ -14,6 +14,7 @@ STRIDE_INF = 0x7FFFFFFF
 MAX_OFFSET = 1 << 24
 MAX_BLOCKS = 7936
 MAX_BATCH_HEADS = 1024
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 PSA_OK = 0
 PSA_ERR_INVALID = 1
@@ -22,7 +23,7 @@ PSA_ERR_WORKSPACE = 3
 PSA_ERR_HIP = 4
 
 EXPORTS = ("psa_num_blocks", "psa_workspace_size", "psa_build_blockmap", "psa_attention_plan",
-           "psa_attention_run", "psa_attention_fwd", "psa_dense_workspace_size", "psa_dense_fwd",
+           "psa_attention_run", "psa_attention_fwd", "psa_attention_fwd_noalloc", "psa_dense_workspace_size", "psa_dense_fwd",
            "psa_blocked_tokens",
            "psa_to_blocks", "psa_from_blocks", "psa_build_blockmap_3d", "psa_workspace_size_3d",
            "psa_attention_plan_3d", "psa_attention_run_3d", "psa_l2_workspace_size", "psa_l2_distance",
@@ -86,6 +87,9 @@ def lib():
         L.psa_attention_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, i32,
                                         ctypes.POINTER(Stripe), ctypes.c_float, vp, sz, vp, vp, vp]
         L.psa_attention_fwd.restype = ctypes.c_int
+        L.psa_attention_fwd_noalloc.argtypes = [vp, vp, vp, vp, i32, i32, i32, Grid, i32,
+                                                ctypes.POINTER(Stripe), ctypes.c_float, vp, vp, vp]
+        L.psa_attention_fwd_noalloc.restype = ctypes.c_int
         L.psa_dense_workspace_size.argtypes = []
         L.psa_dense_workspace_size.restype = sz
         L.psa_dense_fwd.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, vp, vp, sz,

@@ -148,9 +148,8 @@ psa_status_t check_attention_shape(int32_t batch, int32_t n_heads, int32_t head_
   return PSA_OK;
 }
 
-// Limits of the scheduler and the workspace, shared by the plans and runs of both layouts.
-psa_status_t check_work(int32_t batch, int32_t n_heads, const void* workspace,
-                        size_t workspace_bytes, const psa::Geometry* g, psa::WorkspaceLayout* wl) {
+// Limits of the scheduler, shared by the plans and runs of both layouts.
+psa_status_t check_limits(int32_t batch, int32_t n_heads, const psa::Geometry* g) {
   if (g->nb > PSA_MAX_BLOCKS)
     return fail(PSA_ERR_UNSUPPORTED, "%d blocks per sequence exceed %d", g->nb, PSA_MAX_BLOCKS);
   if ((int64_t)batch * n_heads > PSA_MAX_BATCH_HEADS)
@@ -158,6 +157,14 @@ psa_status_t check_work(int32_t batch, int32_t n_heads, const void* workspace,
                 PSA_MAX_BATCH_HEADS);
   if ((int64_t)batch * n_heads * g->nb >= ((int64_t)1 << 31))
     return fail(PSA_ERR_UNSUPPORTED, "too many work items");
+  return PSA_OK;
+}
+
+// Limits of the scheduler and the workspace, shared by the plans and runs of both layouts.
+psa_status_t check_work(int32_t batch, int32_t n_heads, const void* workspace,
+                        size_t workspace_bytes, const psa::Geometry* g, psa::WorkspaceLayout* wl) {
+  const psa_status_t s = check_limits(batch, n_heads, g);
+  if (s != PSA_OK) return s;
   *wl = psa::workspace_layout(batch, n_heads, g->nb, g->pbt > 0);
   if (!workspace || workspace_bytes < wl->total)
     return fail(PSA_ERR_WORKSPACE, "workspace of %zu bytes at %p; %zu bytes required", workspace_bytes,
@@ -417,6 +424,37 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
   if (s != PSA_OK) return s;
   return psa_attention_run(q, k, v, o, batch, n_heads, head_dim, grid, block, softmax_scale,
                            workspace, workspace_bytes, lse, stream);
+}
+
+psa_status_t psa_attention_fwd_noalloc(const void* q, const void* k, const void* v, void* o,
+                                       int32_t batch, int32_t n_heads, int32_t head_dim,
+                                       psa_grid_t grid, int32_t block, const psa_stripe_t* params,
+                                       float softmax_scale, float* lse, int32_t* kept_per_row,
+                                       hipStream_t stream) {
+  // Everything is validated before the first HIP call.
+  psa_status_t s = check_tensors(q, k, v, o, lse);
+  if (s != PSA_OK) return s;
+  s = check_attention_shape(batch, n_heads, head_dim, block);
+  if (s != PSA_OK) return s;
+  psa::Geometry g;
+  if (!grid_geometry(grid, block, &g))
+    return fail(PSA_ERR_INVALID, "invalid grid (%d x %d x %d + %d text)", grid.frames, grid.height,
+                grid.width, grid.n_text);
+  s = check_limits(batch, n_heads, &g);
+  if (s != PSA_OK) return s;
+  s = check_params(params, n_heads);
+  if (s != PSA_OK) return s;
+  s = check_counts_out(kept_per_row, nullptr);
+  if (s != PSA_OK) return s;
+  const size_t need = psa::workspace_layout(batch, n_heads, g.nb, false).total;
+  if (need > PSA_NOALLOC_SCRATCH_BYTES)
+    return fail(PSA_ERR_WORKSPACE, "the plan of these sizes needs %zu bytes; the static scratch holds %zu",
+                need, (size_t)PSA_NOALLOC_SCRATCH_BYTES);
+  void* scratch = nullptr;
+  const hipError_t e = psa::scratch_pointer(&scratch);
+  if (e != hipSuccess) return hip_fail(e, "psa_attention_fwd_noalloc: address of the static scratch");
+  return psa_attention_fwd(q, k, v, o, batch, n_heads, head_dim, grid, block, params, softmax_scale,
+                           scratch, PSA_NOALLOC_SCRATCH_BYTES, lse, kept_per_row, stream);
 }
 
 size_t psa_dense_workspace_size(void) { return psa::kDenseWorkspaceBytes; }

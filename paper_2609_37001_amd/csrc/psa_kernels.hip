@@ -36,6 +36,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "psa_launch.h"
 
 namespace psa {
@@ -1894,6 +1896,39 @@ hipError_t launch_dense(const void* q, const void* k, const void* v, void* o, fl
   if (head_dim == 64 && block == 128)
     return launch_dense_t<64, 128>(q, k, v, o, lse, n_bh, n_tokens, c, queues, w, stream);
   return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Static scratch of psa_attention_fwd_noalloc: the plan of a call lives in this array instead of
+// a caller's workspace.  Every GPU the library runs on holds its own copy, from the time the
+// library's code is loaded on it until the process ends.  In host code `scratch` names a host-side
+// stand-in, not a device address: the kernels only ever get the address scratch_pointer() looked
+// up for the current device.
+// ---------------------------------------------------------------------------------------------
+
+static __device__ __align__(256) uint8_t scratch[PSA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_lock;
+void* g_scratch_address[kMaxDevices];      // per device, once looked up
+}  // namespace
+
+hipError_t scratch_pointer(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_lock);
+  if (!g_scratch_address[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));       // device `dev` is current
+    if (e != hipSuccess) return e;
+    if (!p || ((uintptr_t)p & 255) != 0) return hipErrorInvalidSymbol;
+    g_scratch_address[dev] = p;
+  }
+  *out = g_scratch_address[dev];
+  return hipSuccess;
 }
 
 }  // namespace psa

@@ -128,4 +128,8 @@ hipError_t launch_dense(const void* q, const void* k, const void* v, void* o, fl
                         int32_t block, float scale_log2, int32_t* queues, int32_t n_workgroups,
                         hipStream_t stream);
 
+// Device address of the static scratch of psa_attention_fwd_noalloc on the current device
+// (PSA_NOALLOC_SCRATCH_BYTES, 256-byte aligned), looked up once per device.
+hipError_t scratch_pointer(void** out);
+
 }  // namespace psa

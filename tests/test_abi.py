@@ -68,6 +68,35 @@ def test_attention_validation_codes():
     assert _attn(batch=1025) == _lib.PSA_ERR_UNSUPPORTED
 
 
+def _noalloc(q=1, o=1, batch=1, heads=1, d=128, grid=(2, 8, 8, 0), block=128, params=None, lse=0, kept=0):
+    L = _lib.lib()
+    params = [(1, 0, INF, 1, 0, INF)] * heads if params is None else params
+    vp = lambda x: ctypes.c_void_p(x) if x else None
+    return L.psa_attention_fwd_noalloc(vp(q * 256), vp(256), vp(256), vp(o * 256), batch, heads, d,
+                                       _lib.grid_of(*grid), block, _lib.stripes(params), 0.1, vp(lse), vp(kept),
+                                       None)
+
+
+def test_noalloc_validation_before_any_hip_call():
+    """Invalid arguments and sizes whose plan exceeds the static scratch are rejected before the
+    entry point touches the GPU (this container has none)."""
+    assert _noalloc(q=0) == _lib.PSA_ERR_INVALID
+    assert _noalloc(d=96) == _lib.PSA_ERR_UNSUPPORTED
+    assert _noalloc(params=[(1, 0, 0, 1, 0, 1)]) == _lib.PSA_ERR_INVALID
+    assert _noalloc(grid=(0, 8, 8, 0)) == _lib.PSA_ERR_INVALID
+    assert _noalloc(lse=2) == _lib.PSA_ERR_INVALID                               # misaligned float
+    assert _noalloc(kept=3) == _lib.PSA_ERR_INVALID                              # misaligned int32
+    assert _noalloc(grid=(100, 100, 128, 0)) == _lib.PSA_ERR_UNSUPPORTED           # 10000 blocks
+    # 1000 heads x 7936 blocks: the plan needs far more than the scratch holds
+    big = (62, 128, 128, 0)
+    need = psa.workspace_size(1, 1000, big, 128)
+    assert need > _lib.NOALLOC_SCRATCH_BYTES
+    assert _noalloc(heads=1000, grid=big) == _lib.PSA_ERR_WORKSPACE
+    assert b"static scratch" in _lib.lib().psa_last_error()
+    # 40 heads of the Wan 2.1 14B grid fit
+    assert psa.workspace_size(1, 40, (21, 45, 80), 128) < _lib.NOALLOC_SCRATCH_BYTES
+
+
 def test_error_messages():
     L = _lib.lib()
     assert _attn(params=[(1, 0, 0, 1, 0, 1)]) == _lib.PSA_ERR_INVALID
