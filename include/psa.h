@@ -186,9 +186,11 @@ psa_status_t psa_attention_fwd_noalloc(const void* q, const void* k, const void*
 /* Bytes of device workspace psa_dense_fwd can use (a constant: queue bounds and counters). */
 size_t psa_dense_workspace_size(void);
 
-/* Dense attention forward with the same tile engine (every block kept): the speedup baseline
- * and the attention of the steps that run dense.  Same tensor layout, with N = n_tokens.  At
- * full density psa_attention_fwd returns the same bits as this call.
+/* Dense attention forward with the same tile engine (every block kept).  Sec. 4, setup: the first
+ * 20 % of the denoising steps keep full attention (FlashAttention-3 in the paper's runs), and the
+ * paper's kernel speedups are quoted against that full attention; this call plays both roles, the
+ * attention of the steps that run dense and the speedup baseline.  Same tensor layout, with
+ * N = n_tokens.  At full density psa_attention_fwd returns the same bits as this call.
  *   workspace      device, psa_dense_workspace_size() bytes or more, 256-byte aligned, or NULL.
  *                  With a workspace a small kernel arms per-XCD work queues in it and a
  *                  persistent grid takes the work items, each workgroup from its own XCD's queue
