@@ -405,7 +405,9 @@ def computed_flops(psa, cfg, params, torch):
 
 
 def cpu_baseline(cfg, params, seconds):
-    """The oracle on the host cores, on a seeded sample of query blocks of the same workload."""
+    """The oracle on the host cores, on a seeded, stratified sample of (head, query block) rows of
+    the same workload: the longest row, the shortest non-empty row, the partial last block, a text
+    block if there is one, then seeded random rows until `seconds` have passed (at most 400)."""
     import oracle
     from threadpoolctl import threadpool_info
     from workloads.inputs import make_head_qkv, rope_tables
@@ -414,21 +416,29 @@ def cpu_baseline(cfg, params, seconds):
     nb = cfg.n_blocks
     lens = np.full(nb, cfg.block, dtype=np.float64)
     lens[-1] = cfg.n_tokens - (nb - 1) * cfg.block
+    picks = [tuple(int(x) for x in np.unravel_index(np.argmax(rows_kept), rows_kept.shape))]
+    masked = np.where(rows_kept > 0, rows_kept, np.iinfo(np.int32).max)
+    picks.append(tuple(int(x) for x in np.unravel_index(np.argmin(masked), rows_kept.shape)))
+    picks.append((cfg.heads - 1, nb - 1))
+    _, _, _, glob_blk = oracle.block_coordinates(cfg.frames, cfg.height, cfg.width, cfg.n_text, cfg.block)
+    if glob_blk.any():
+        picks.append((0, int(np.nonzero(glob_blk)[0][0])))
     rng = np.random.default_rng(12345)
-    heads = rng.choice(cfg.heads, size=min(4, cfg.heads), replace=False)
+    heads = sorted({h for h, _ in picks} | {int(x) for x in rng.choice(cfg.heads, size=min(4, cfg.heads),
+                                                                       replace=False)})
     tables = rope_tables(cfg)
-    data = {int(h): make_head_qkv(cfg, 0, int(h), tables) for h in heads}
+    data = {h: make_head_qkv(cfg, 0, h, tables) for h in heads}        # inputs, not timed
     flops = 0.0
-    n_blocks = 0
+    done = []
     t0 = time.perf_counter()
-    while time.perf_counter() - t0 < seconds and n_blocks < 400:
-        h = int(heads[n_blocks % len(heads)])
-        qb = int(rng.integers(nb))
+    while len(done) < 400 and (len(done) < len(picks) or time.perf_counter() - t0 < seconds):
+        h, qb = picks[len(done)] if len(done) < len(picks) else (heads[int(rng.integers(len(heads)))],
+                                                                 int(rng.integers(nb)))
         q, k, v = data[h]
         rows = np.arange(qb * cfg.block, min(cfg.n_tokens, (qb + 1) * cfg.block))
         oracle.masked_attention(q, k, v, bmap[h], cfg.block, cfg.scale, rows)
         flops += 4.0 * cfg.head_dim * lens[qb] * float((bmap[h, qb] * lens).sum())
-        n_blocks += 1
+        done.append((h, qb))
     elapsed = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     full = 4.0 * cfg.head_dim * cfg.batch * float((bmap * lens[None, :, None] * lens[None, None, :]).sum())
@@ -438,11 +448,13 @@ def cpu_baseline(cfg, params, seconds):
         "cores": int(threads),
         "kind": "oracle",
         "extrapolated_full_step_s": round(full / (flops / elapsed), 1),
-        "sample": "%d query blocks of 128 rows from heads %s of the same workload (float64 numpy "
-                  "oracle, %.1f s, %d host cores visible); %.3g TFLOP computed, mean %.1f kept "
-                  "blocks per sampled row" % (n_blocks, sorted(int(x) for x in heads), elapsed,
-                                              os.cpu_count() or 0, flops / 1e12,
-                                              float(rows_kept[heads].mean())),
+        "sample": "%d (head, query block) rows of %d tokens of the same workload, stratified (longest row, "
+                  "shortest non-empty row, partial last block%s, then seeded random rows), each computed in "
+                  "full by the float64 numpy oracle in %.1f s with %d BLAS threads (%d host cores visible); "
+                  "%.3g TFLOP, mean %.1f kept blocks per sampled row; random rows from heads %s"
+                  % (len(done), cfg.block, ", a text block" if glob_blk.any() else "", elapsed, threads,
+                     os.cpu_count() or 0, flops / 1e12, float(np.mean([rows_kept[h, qb] for h, qb in done])),
+                     heads),
     }
 
 

@@ -8,7 +8,8 @@ import ctypes
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libpsa.so")
+# PSA_LIBRARY selects another build of the library (the host-sanitized one of build.py --asan).
+LIB_PATH = os.environ.get("PSA_LIBRARY") or os.path.join(PKG, "libpsa.so")
 
 STRIDE_INF = 0x7FFFFFFF
 MAX_OFFSET = 1 << 24
