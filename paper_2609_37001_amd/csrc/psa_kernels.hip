@@ -1529,7 +1529,8 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 // block of a work item, waves 4-7 the second (each wave 32 rows, the per-wave tile engine
 // above).  The two rows share one stream of K/V blocks -- the union of their kept sets, each
 // entry marked with the rows that keep it -- double-buffered in LDS with one barrier per block
-// and every block's loads issued a whole block ahead; a row skips the blocks it does not keep.
+// and every block's loads issued during the block before (K after its barrier, V after its
+// first Q K^T half); a row skips the blocks it does not keep.
 // The plan pairs rows with equal kept sets, so a K/V block is loaded once for two query blocks
 // and most entries are used by both rows.  Each row still visits its own kept blocks in
 // ascending order with the same arithmetic, so its output is that of the one-row engine.
@@ -1656,14 +1657,17 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
   auto entry = [&](int i) {
     return SPARSE ? (int)__builtin_amdgcn_readfirstlane(list[i]) : (i | (3 << kEntryRowShift));
   };
-  auto issue = [&](int buf, int kb) {
+  auto issue_k = [&](int buf, int kb) {
     issue_block8<D, BLK>(plan, kh, lds_address(sk[buf]), lds_address(sk[buf]) + HALF, kb, n);
+  };
+  auto issue_v = [&](int buf, int kb) {
     issue_block8<D, BLK>(plan, vh, lds_address(sv[buf]), lds_address(sv[buf]) + HALF, kb, n);
   };
   int e = 0;
   if (nu > 0) {
     e = entry(0);
-    issue(0, e & kEntryBlockMask);
+    issue_k(0, e & kEntryBlockMask);
+    issue_v(0, e & kEntryBlockMask);
   }
   for (int i = 0; i < nu; i++) {
     const int kb = e & kEntryBlockMask;
@@ -1679,18 +1683,28 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
     }
     wait_dma<0>();                                        // block i, issued a block ago
     __syncthreads();                                      // ... by every wave; block i-1 read
-    if (i + 1 < nu) {
+    // The next block's K goes out right after the barrier and its V after this block's first
+    // Q K^T half: a wave stalls while it issues, and a single burst of all its loads after the
+    // barrier, where every wave issues at once, keeps the MFMA pipes idle for longer (measured:
+    // sparse 0.5-1.3 % and dense 0.4-3 % faster on two boxes, same bits).
+    const bool more = i + 1 < nu;
+    int kbn = 0;
+    if (more) {
       e = entry(i + 1);
-      issue((i + 1) & 1, e & kEntryBlockMask);
+      kbn = e & kEntryBlockMask;
+      issue_k((i + 1) & 1, kbn);
     }
     if (mine) {
       const uint8_t* skb = sk[i & 1];
       const uint8_t* svb = sv[i & 1];
       f32x16 s[H::KT];
       qk_half<D, BLK>(st, s, skb, 0, lane);
+      if (more) issue_v((i + 1) & 1, kbn);
       softmax_pv_half<D, BLK, PAD>(st, s, svb, kb, 0, n, tail, lo, hi, lane);
       qk_half<D, BLK>(st, s, skb, H::HK, lane);
       softmax_pv_half<D, BLK, PAD>(st, s, svb, kb, H::HK, n, tail, lo, hi, lane);
+    } else if (more) {
+      issue_v((i + 1) & 1, kbn);
     }
   }
   if (my_row >= 0) store_rows<D, BLK>(st, oh, lseh, row, n, lane);
@@ -1700,15 +1714,26 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
 // pairs (2 p, 2 p + 1) of the flattened (batch*head, pair) list, either popped from armed queues
 // by a persistent grid (queues given) or one pair per workgroup, consecutive workgroups of one
 // XCD taking consecutive pairs.
+// Byte offsets of the plan's sections in the workspace handed to the pair engine (a workspace of
+// up to 4 GiB: one base pointer and 32-bit offsets keep fewer kernel arguments live in scalar
+// registers than one pointer per section).
+struct PlanView {
+  uint32_t params, coords, order, queues, masks, pairs;
+};
+
 template <int D, int BLK, bool SPARSE, bool PAD>
 __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2))) void psa_pair_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-    __bf16* __restrict__ o, float* __restrict__ lse, const psa_stripe_t* __restrict__ params,
-    const int2* __restrict__ coords, const int32_t* __restrict__ order,
-    int32_t* __restrict__ queues, const uint64_t* __restrict__ masks,
-    const int2* __restrict__ pairs, const PlanHeader* __restrict__ header, PlanHeader expect,
-    float c) {
+    __bf16* __restrict__ o, float* __restrict__ lse, const uint8_t* __restrict__ ws, PlanView pv,
+    PlanHeader expect, float c) {
   using T = Tile<D, BLK>;
+  const PlanHeader* header = (const PlanHeader*)ws;
+  const psa_stripe_t* params = (const psa_stripe_t*)(ws + pv.params);
+  const int2* coords = (const int2*)(ws + pv.coords);
+  const int32_t* order = (const int32_t*)(ws + pv.order);
+  int32_t* queues = ws ? (int32_t*)(ws + pv.queues) : nullptr;
+  const uint64_t* masks = (const uint64_t*)(ws + pv.masks);
+  const int2* pairs = (const int2*)(ws + pv.pairs);
   static_assert(T::kWaves == 4, "a row is four waves");
   __shared__ __attribute__((aligned(1024))) uint8_t sk[2][T::BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sv[2][T::BYTES];
@@ -1803,12 +1828,12 @@ static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, v
   if (e != hipSuccess) return e;
   if constexpr (BLK == 128) {
     // one eight-wave pair workgroup per CU
+    static_assert(sizeof(PlanHeader) <= 256, "the plan header is the workspace's first section");
+    const PlanView pv = {(uint32_t)wl.params, (uint32_t)wl.coords, (uint32_t)wl.order, (uint32_t)wl.queues,
+                         (uint32_t)(PAD ? wl.masks : 0), (uint32_t)wl.pairs};
     hipLaunchKernelGGL((psa_pair_kernel<D, BLK, true, PAD>), dim3(n_wg / 2), dim3(4 * BLK), 0, stream,
                        (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
-                       (const psa_stripe_t*)(ws + wl.params), (const int2*)(ws + wl.coords),
-                       (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues),
-                       PAD ? (const uint64_t*)(ws + wl.masks) : nullptr, (const int2*)(ws + wl.pairs),
-                       (const PlanHeader*)(ws + wl.header), expect, c);
+                       (const uint8_t*)ws, pv, expect, c);
   } else {
     hipLaunchKernelGGL((psa_sparse_kernel<D, BLK, PAD>), dim3(n_wg), dim3(Tile<D, BLK>::kThreads), 0, stream,
                        (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
@@ -1869,9 +1894,10 @@ static hipError_t launch_dense_t(const void* q, const void* k, const void* v, vo
     e.nb = nb;
     e.n = n;
     const int32_t grid = queues ? n_wg / 2 : per_xcd * kNumQueues;
+    const PlanView pv = {0, 0, 0, 0, 0, 0};         // the dense workspace is the queue area
     hipLaunchKernelGGL((psa_pair_kernel<D, BLK, false, false>), dim3(grid), dim3(4 * BLK), 0, stream,
-                       (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse, nullptr,
-                       nullptr, nullptr, queues, nullptr, nullptr, nullptr, e, c);
+                       (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
+                       (const uint8_t*)queues, pv, e, c);
   } else {
     const int32_t grid = queues ? n_wg : per_xcd * kNumQueues;
     hipLaunchKernelGGL((psa_dense_kernel<D, BLK>), dim3(grid), dim3(Tile<D, BLK>::kThreads), 0, stream,
