@@ -122,7 +122,11 @@ psa_status_t psa_build_blockmap(const psa_stripe_t* params, int32_t n_heads, psa
  * in index order) and weighed by the union of the two sets.  Order: items
  * of more than three times the mean work (rows that keep every key block, such as text rows)
  * first, longest first, then the heads longest first, each split into equal-work ranges, one
- * work queue per XCD.  The plan
+ * work queue per XCD.  At block 128 the plan also chooses where each pair item's K/V stream
+ * starts (each row still visits each of its kept blocks once, cyclically ascending from there):
+ * where the item started just before it on its queue is predicted to be by then, so that the items
+ * in flight on one XCD read the same key blocks at about the same time and its L2 serves them
+ * once; pairs that keep every block start at block 0.  The plan
  * depends only on the sizes and on params, so one plan serves any number of runs (a layer's
  * stripes stay fixed over the denoising steps).
  *   workspace     device, psa_workspace_size(batch, n_heads, grid, block) bytes or more,

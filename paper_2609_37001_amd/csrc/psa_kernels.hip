@@ -7,6 +7,7 @@
 //                                              and kept-set signatures for the pairing
 //   psa_pairing_kernel / psa_paircount_kernel  pairs of query blocks (block 128) and their work
 //   psa_schedule_kernel                        load-balanced work order split over 8 XCD queues
+//   psa_starts_kernel                          block 128: where each pair item's K/V stream starts
 //   psa_pair_kernel                            block 128: persistent block-sparse attention
 //                                              (Algorithm 2) on pairs of query blocks, or dense
 //   psa_sparse_kernel / psa_dense_kernel       block 64: the same with one query block per item
@@ -359,7 +360,11 @@ WorkspaceLayout workspace_layout(int32_t batch, int32_t n_heads, int32_t nb, boo
   wl.queues = up(wl.order + sizeof(int32_t) * items);
   wl.sigs = up(wl.queues + sizeof(int32_t) * kQueueWords);
   wl.pairs = up(wl.sigs + sizeof(uint64_t) * (size_t)n_heads * nb);
-  wl.masks = up(wl.pairs + sizeof(int2) * (size_t)n_heads * pairs_per_head(nb));
+  const size_t pair_items = (size_t)batch * n_heads * pairs_per_head(nb);
+  wl.spans = up(wl.pairs + sizeof(int2) * (size_t)n_heads * pairs_per_head(nb));
+  wl.runspans = up(wl.spans + sizeof(uint32_t) * pair_items);
+  wl.starts = up(wl.runspans + sizeof(uint32_t) * pair_items);
+  wl.masks = up(wl.starts + sizeof(int32_t) * pair_items);
   wl.total = masks ? up(wl.masks + 2 * sizeof(uint64_t) * (size_t)nb) : wl.masks;
   return wl;
 }
@@ -617,11 +622,14 @@ __global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __res
     if (partner[i] >= -1 && run[i] < pairs_per_head(nb)) dst[run[i]] = make_int2(i, partner[i]);
 }
 
-// One wave per pair item (batch, head, pair): number of key blocks kept by either row.
+// One wave per pair item (batch, head, pair): number of key blocks kept by either row, and the
+// first and last of them that are not global (video blocks; the span the start of the item's
+// stream is placed in).
 __global__ __launch_bounds__(256) void psa_paircount_kernel(const psa_stripe_t* __restrict__ params,
                                                             const int2* __restrict__ coords,
                                                             const int2* __restrict__ pairs,
                                                             int32_t* __restrict__ counts,
+                                                            uint32_t* __restrict__ spans,
                                                             int32_t n_items, int32_t n_heads,
                                                             int32_t nb) {
   const int32_t np = pairs_per_head(nb);
@@ -632,13 +640,25 @@ __global__ __launch_bounds__(256) void psa_paircount_kernel(const psa_stripe_t* 
   const int2 pr = pairs[(int64_t)h * np + p];
   const int2 ca = coords[pr.x];
   const int2 cb = pr.y >= 0 ? coords[pr.y] : make_int2(kDeadTile, 0);
-  int cnt = 0;
+  int cnt = 0, lo = nb, hi = -1;
   for (int32_t kb = lane; kb < nb; kb += 64) {
     const int2 ck = coords[kb];
-    cnt += (tile_keep(m, ca, ck) || tile_keep(m, cb, ck)) ? 1 : 0;
+    const bool keep = tile_keep(m, ca, ck) || tile_keep(m, cb, ck);
+    cnt += keep ? 1 : 0;
+    if (keep && ck.x >= 0) {
+      lo = min(lo, kb);
+      hi = max(hi, kb);
+    }
   }
   cnt = wave_sum(cnt);
-  if (lane == 0) counts[item] = cnt;
+  for (int off = 32; off > 0; off >>= 1) {
+    lo = min(lo, __shfl_xor(lo, off));
+    hi = max(hi, __shfl_xor(hi, off));
+  }
+  if (lane == 0) {
+    counts[item] = cnt;
+    spans[item] = hi < 0 ? 0xffffffffu : ((uint32_t)lo | ((uint32_t)hi << 16));
+  }
 }
 
 // Work estimate of an item, in tiles: kept key blocks plus a fixed cost for loading Q,
@@ -664,7 +684,10 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
                                                             int32_t* __restrict__ order,
                                                             int32_t* __restrict__ queues,
                                                             PlanHeader* __restrict__ header,
-                                                            PlanHeader done, int32_t nb) {
+                                                            PlanHeader done, int32_t nb,
+                                                            int32_t write_header,
+                                                            const uint32_t* __restrict__ spans,
+                                                            uint32_t* __restrict__ runspans) {
   const int32_t n_bh = done.n_bh, n = n_bh * nb;
   __shared__ int64_t total[PSA_MAX_BATCH_HEADS];
   __shared__ int32_t by_rank[PSA_MAX_BATCH_HEADS];
@@ -863,6 +886,7 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
     if (valid) {
       const int32_t pos = base + __builtin_popcountll(same & ((1ull << lane) - 1));
       order[qstart[pos % kNumQueues] + pos / kNumQueues] = item;
+      if (runspans) runspans[item] = spans[item];        // a long item is a run of its own
       if (__builtin_ctzll(same) == lane) hist[wave][cls] = base + __builtin_popcountll(same);
     }
     __builtin_amdgcn_wave_barrier();
@@ -871,19 +895,181 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
     const int32_t r = pair / kNumQueues, x = pair - r * kNumQueues;
     const int32_t item0 = by_rank[r] * nb, end = bounds[r][x + 1];
     int32_t* dst = order + qstart[x] + qoff[r][x];
+    uint32_t lo = 0xffffu, hi = 0;
     for (int32_t qb = bounds[r][x] + lane; __builtin_amdgcn_readfirstlane(qb - lane) < end; qb += 64) {
       const bool keep = qb < end && !is_long(item0 + qb);
       const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
       if (keep) dst[__builtin_popcountll(mask & ((1ull << lane) - 1))] = item0 + qb;
       dst += __builtin_popcountll(mask);
+      if (runspans && keep && spans[item0 + qb] != 0xffffffffu) {
+        lo = min(lo, spans[item0 + qb] & 0xffffu);
+        hi = max(hi, spans[item0 + qb] >> 16);
+      }
+    }
+    if (runspans) {
+      // the run's span: the union of its items' spans of non-global blocks
+      for (int off = 32; off > 0; off >>= 1) {
+        lo = min(lo, (uint32_t)__shfl_xor((int32_t)lo, off));
+        hi = max(hi, (uint32_t)__shfl_xor((int32_t)hi, off));
+      }
+      const uint32_t run = lo > hi ? 0xffffffffu : (lo | (hi << 16));
+      for (int32_t qb = bounds[r][x] + lane; qb < end; qb += 64)
+        if (!is_long(item0 + qb)) runspans[item0 + qb] = run;
     }
   }
   if (tid <= kNumQueues) queues[tid] = qstart[tid];
   if (tid < kNumQueues) queues[kQueueCounters + tid * kCounterStride] = 0;
+  if (tid == 0) queues[kStartsDone] = 0;
   __syncthreads();
-  if (tid == 0) {
+  if (tid == 0 && write_header) {
     __threadfence();
     *header = done;
+  }
+}
+
+// Where each pair item's K/V stream starts (one wave per work queue).  The workgroups of one XCD
+// share its L2, and a K/V block stays there for only about two block steps of the XCD's 32
+// workgroups; so a block is reused only when the items in flight on the XCD read it at nearly
+// the same time.  Each item therefore starts its cyclic walk over its key blocks where the item
+// started just before it on the same queue is predicted to be by then: this wave replays the
+// queue with 32 workgroups taking items as they become free (work = kept blocks + item overhead,
+// the schedule's estimate), keeping the 32 times at which they become free sorted over its lanes,
+// and places the predecessor's position by linear interpolation over the predecessor's span of
+// non-global key blocks.  Items that keep every key block start at block 0 (ascending, as in the
+// dense kernel).  The result depends on the plan only, so runs stay deterministic.
+// One single-wave workgroup per queue; the last workgroup to finish writes the plan header.
+//  1. Start times: the 32 times at which the XCD's workgroups become free are kept sorted over
+//     lanes 0..31; the queue's items are replayed 16 at a time -- they start at the 16 earliest
+//     free times (this differs from taking them one by one only when an item of the group would
+//     end before a later one of the group starts), their workgroups' next free times replace those
+//     lanes, and a bitonic sort over the 32 lanes restores the order.  Each item's start time is
+//     kept in `starts` for step 2.
+//  2. Start blocks: within a run (the items of one head's range in the queue), each item starts
+//     where its predecessor is predicted to be by then: the predecessor's start block advanced by
+//     (its elapsed time / its work) of the run's span, cyclically; a run's first item starts at
+//     its own first non-global block.  These are prefix sums over each run, 64 items at a time.
+// Items that keep every key block start at block 0 (ascending, as in the dense kernel).
+constexpr int kStartGroup = 16;
+constexpr uint32_t kNoSpan = 0xffffffffu;
+
+// Lane i receives lane i ^ m of x (m = 1, 2, 4, 8 by DPP within a 16-lane row; 16 by a shuffle).
+template <int M>
+__device__ __forceinline__ int32_t lane_xor(int32_t x, int lane) {
+  if constexpr (M == 1) return __builtin_amdgcn_update_dpp(x, x, 0xb1, 0xf, 0xf, false);  // quad_perm 1,0,3,2
+  if constexpr (M == 2) return __builtin_amdgcn_update_dpp(x, x, 0x4e, 0xf, 0xf, false);  // quad_perm 2,3,0,1
+  if constexpr (M == 4) {
+    const int32_t fwd = __builtin_amdgcn_update_dpp(x, x, 0x104, 0xf, 0xf, false);      // row_shl:4
+    const int32_t bwd = __builtin_amdgcn_update_dpp(x, x, 0x114, 0xf, 0xf, false);      // row_shr:4
+    return (lane & 4) ? bwd : fwd;
+  }
+  if constexpr (M == 8) return __builtin_amdgcn_update_dpp(x, x, 0x128, 0xf, 0xf, false); // row_ror:8
+  return __shfl_xor(x, M);
+}
+
+template <int K, int H>
+__device__ __forceinline__ int32_t bitonic_step(int32_t v, int lane) {
+  const int32_t other = lane_xor<H>(v, lane);
+  const bool up = ((lane & K) == 0) == ((lane & H) == 0);
+  return up ? min(v, other) : max(v, other);
+}
+
+__global__ __launch_bounds__(64) void psa_starts_kernel(
+    const int32_t* __restrict__ counts, const uint32_t* __restrict__ spans,
+    const uint32_t* __restrict__ runspans, const int32_t* __restrict__ order,
+    int32_t* __restrict__ queues, int32_t* __restrict__ starts, PlanHeader* __restrict__ header,
+    PlanHeader done, int32_t np, int32_t nb) {
+  constexpr int kSlots = 32;                       // workgroups of one XCD
+  const int lane = threadIdx.x, queue = blockIdx.x;
+  const int32_t q0 = queues[queue], q1 = queues[queue + 1];
+
+  // 1. Start times (lanes 32..63 hold INT32_MAX and stay in place).
+  int32_t free_at = lane < kSlots ? 0 : INT32_MAX;
+  for (int32_t base = q0; base < q1; base += kStartGroup) {
+    const int gn = min(kStartGroup, q1 - base);
+    const bool mine = lane < gn;
+    const int32_t item = mine ? order[base + lane] : 0;
+    const int32_t work = mine ? counts[item] + kItemOverhead : 0;
+    if (mine) starts[item] = free_at;              // lane i: the i-th earliest free time
+    free_at += work;
+    free_at = bitonic_step<2, 1>(free_at, lane);
+    free_at = bitonic_step<4, 2>(free_at, lane);
+    free_at = bitonic_step<4, 1>(free_at, lane);
+    free_at = bitonic_step<8, 4>(free_at, lane);
+    free_at = bitonic_step<8, 2>(free_at, lane);
+    free_at = bitonic_step<8, 1>(free_at, lane);
+    free_at = bitonic_step<16, 8>(free_at, lane);
+    free_at = bitonic_step<16, 4>(free_at, lane);
+    free_at = bitonic_step<16, 2>(free_at, lane);
+    free_at = bitonic_step<16, 1>(free_at, lane);
+    free_at = bitonic_step<32, 16>(free_at, lane);
+    free_at = bitonic_step<32, 8>(free_at, lane);
+    free_at = bitonic_step<32, 4>(free_at, lane);
+    free_at = bitonic_step<32, 2>(free_at, lane);
+    free_at = bitonic_step<32, 1>(free_at, lane);
+    free_at = lane < kSlots ? free_at : INT32_MAX;
+  }
+  __threadfence_block();                            // step 2 reads what step 1 wrote
+
+  // 2. Start blocks: segmented prefix sums over the runs, 64 items at a time.
+  int32_t c_bh = -1, c_start = 0, c_work = 1;       // the item before this chunk
+  uint32_t c_run = kNoSpan;
+  int64_t c_acc = 0;                                 // the running sum at that item
+  for (int32_t base = q0; base < q1; base += 64) {
+    const int32_t idx = base + lane;
+    const bool live = idx < q1;
+    const int32_t item = live ? order[idx] : 0;
+    const int32_t bh = item / np;
+    const int32_t cnt = live ? counts[item] : 0;
+    const uint32_t own = live ? spans[item] : kNoSpan;
+    const uint32_t run = live ? runspans[item] : kNoSpan;
+    const int32_t t = live ? starts[item] : 0;
+    // the previous item of the queue
+    int32_t p_bh = __shfl_up(bh, 1), p_t = __shfl_up(t, 1), p_work = __shfl_up(cnt, 1) + kItemOverhead;
+    uint32_t p_run = (uint32_t)__shfl_up((int32_t)run, 1);
+    if (lane == 0) {
+      p_bh = c_bh;
+      p_t = c_start;
+      p_work = c_work;
+      p_run = c_run;
+    }
+    const bool first = p_bh != bh || p_run != run || idx == q0;
+    const int32_t lo = (int32_t)(run & 0xffffu), len = (int32_t)(run >> 16) - lo + 1;
+    int64_t v = 0;
+    if (run != kNoSpan) {
+      if (first)
+        v = own != kNoSpan ? (int64_t)(own & 0xffffu) - lo : 0;
+      else
+        v = (int64_t)min(max(t - p_t, 0), p_work - 1) * len / p_work;
+    }
+    // segmented inclusive scan (a segment starts at `first`; lane 0 continues the carry)
+    int64_t acc = v;
+    bool head = first;
+    if (lane == 0 && !first) acc += c_acc;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int64_t a = __shfl_up(acc, off);
+      const int hs = __shfl_up((int)head, off);
+      if (lane >= off && !head) {
+        acc += a;
+        head = hs != 0;
+      }
+    }
+    int32_t kb = run == kNoSpan ? 0 : lo + (int32_t)(acc % len);
+    if (cnt >= nb) kb = 0;
+    if (live) starts[item] = kb;
+    // carry: the last live item of the chunk
+    const int lastl = min(64, q1 - base) - 1;
+    c_bh = __shfl(bh, lastl);
+    c_start = __shfl(t, lastl);
+    c_work = __shfl(cnt, lastl) + kItemOverhead;
+    c_run = (uint32_t)__shfl((int32_t)run, lastl);
+    c_acc = __shfl(acc, lastl);
+  }
+  if (lane == 0) {
+    __threadfence();
+    if (atomicAdd(&queues[kStartsDone], 1) == kNumQueues - 1) {
+      __threadfence();
+      *header = done;
+    }
   }
 }
 
@@ -930,7 +1116,8 @@ hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, vo
     per_head = pairs_per_head(g.nb);
     const int32_t n_items = batch * n_heads * per_head;
     hipLaunchKernelGGL(psa_paircount_kernel, dim3((n_items + 3) / 4), dim3(256), 0, stream, params, coords,
-                       (const int2*)(ws + wl.pairs), counts, n_items, n_heads, g.nb);
+                       (const int2*)(ws + wl.pairs), counts, (uint32_t*)(ws + wl.spans), n_items, n_heads,
+                       g.nb);
   } else {
     const int32_t n_items = batch * n_heads * g.nb;
     hipLaunchKernelGGL(psa_count_kernel, dim3((n_items + 3) / 4), dim3(256), 0, stream, params, coords,
@@ -939,7 +1126,14 @@ hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, vo
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(psa_schedule_kernel, dim3(1), dim3(1024), 0, stream, (const int32_t*)counts,
                      (int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues), (PlanHeader*)(ws + wl.header),
-                     plan_header(g, batch, n_heads), per_head);
+                     plan_header(g, batch, n_heads), per_head, (int32_t)!pair_engine(g),
+                     pair_engine(g) ? (const uint32_t*)(ws + wl.spans) : nullptr,
+                     pair_engine(g) ? (uint32_t*)(ws + wl.runspans) : nullptr);
+  if ((e = hipGetLastError()) != hipSuccess || !pair_engine(g)) return e;
+  hipLaunchKernelGGL(psa_starts_kernel, dim3(kNumQueues), dim3(64), 0, stream, (const int32_t*)counts,
+                     (const uint32_t*)(ws + wl.spans), (const uint32_t*)(ws + wl.runspans),
+                     (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues), (int32_t*)(ws + wl.starts),
+                     (PlanHeader*)(ws + wl.header), plan_header(g, batch, n_heads), per_head, g.nb);
   return hipGetLastError();
 }
 
@@ -1532,8 +1726,9 @@ __global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 // and every block's loads issued during the block before (K after its barrier, V after its
 // first Q K^T half); a row skips the blocks it does not keep.
 // The plan pairs rows with equal kept sets, so a K/V block is loaded once for two query blocks
-// and most entries are used by both rows.  Each row still visits its own kept blocks in
-// ascending order with the same arithmetic, so its output is that of the one-row engine.
+// and most entries are used by both rows.  Each row visits each of its own kept blocks once,
+// with the one-row engine's arithmetic; the stream runs cyclically from a block the plan chooses
+// (psa_starts_kernel), and from block 0 for pairs that keep every block.
 // ---------------------------------------------------------------------------------------------
 
 // Direct global->LDS loads of a whole K or V block by the eight waves of a workgroup: wave w
@@ -1626,8 +1821,9 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
                                              const __bf16* __restrict__ kh,
                                              const __bf16* __restrict__ vh,
                                              __bf16* __restrict__ oh, float* __restrict__ lseh,
-                                             int n, int my_row, int nu, const uint16_t* list,
-                                             float c, uint8_t (*sk)[Tile<D, BLK>::BYTES],
+                                             int n, int my_row, int nu, int first,
+                                             const uint16_t* list, float c,
+                                             uint8_t (*sk)[Tile<D, BLK>::BYTES],
                                              uint8_t (*sv)[Tile<D, BLK>::BYTES],
                                              const uint64_t* masks) {
   using T = Tile<D, BLK>;
@@ -1654,8 +1850,15 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
 #pragma unroll
   for (int dt = 0; dt < T::DT; dt++) st.o[dt] = (f32x16){};
 
+  // Entry i of the stream: list entry first + i, cyclically.
   auto entry = [&](int i) {
-    return SPARSE ? (int)__builtin_amdgcn_readfirstlane(list[i]) : (i | (3 << kEntryRowShift));
+    if constexpr (SPARSE) {
+      int j = i + first;
+      j = j >= nu ? j - nu : j;
+      return (int)__builtin_amdgcn_readfirstlane(list[j]);
+    } else {
+      return i | (3 << kEntryRowShift);
+    }
   };
   auto issue_k = [&](int buf, int kb) {
     issue_block8<D, BLK>(plan, kh, lds_address(sk[buf]), lds_address(sk[buf]) + HALF, kb, n);
@@ -1718,7 +1921,7 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
 // up to 4 GiB: one base pointer and 32-bit offsets keep fewer kernel arguments live in scalar
 // registers than one pointer per section).
 struct PlanView {
-  uint32_t params, coords, order, queues, masks, pairs;
+  uint32_t params, coords, order, queues, masks, pairs, starts;
 };
 
 template <int D, int BLK, bool SPARSE, bool PAD>
@@ -1734,11 +1937,12 @@ __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
   int32_t* queues = ws ? (int32_t*)(ws + pv.queues) : nullptr;
   const uint64_t* masks = (const uint64_t*)(ws + pv.masks);
   const int2* pairs = (const int2*)(ws + pv.pairs);
+  const int32_t* starts = (const int32_t*)(ws + pv.starts);
   static_assert(T::kWaves == 4, "a row is four waves");
   __shared__ __attribute__((aligned(1024))) uint8_t sk[2][T::BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t sv[2][T::BYTES];
   __shared__ uint16_t list[SPARSE ? PSA_MAX_BLOCKS : 1];
-  __shared__ int32_t misc[16];
+  __shared__ int32_t misc[24];
 
   if constexpr (SPARSE) {
     // A workspace without a finished plan for exactly these sizes is left alone.
@@ -1780,12 +1984,15 @@ __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
     const int my_row = __builtin_amdgcn_readfirstlane(grp == 0 ? pr.x : pr.y);
 
-    int32_t nu = nb;
+    int32_t nu = nb, first = 0;
     if constexpr (SPARSE) {
-      // In-kernel decode of the union of the two rows' kept key blocks (ascending).
+      // In-kernel decode of the union of the two rows' kept key blocks (ascending), and the
+      // number of them below the block the plan starts this item's stream at (the stream then
+      // runs cyclically from there).
       const psa_stripe_t m = params[h];
       const int2 ca = coords[pr.x];
       const int2 cb = pr.y >= 0 ? coords[pr.y] : make_int2(kDeadTile, 0);
+      const int32_t start = starts[item];
       nu = 0;
       for (int32_t base = 0; base < nb; base += 8 * 64) {
         const int32_t kb = base + tid;
@@ -1793,13 +2000,18 @@ __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
         const bool ka = tile_keep(m, ca, ck), kbk = tile_keep(m, cb, ck);
         const bool keep = ka || kbk;
         const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
-        if (lane == 0) misc[wave] = __builtin_popcountll(mask);
+        const uint64_t below = __builtin_amdgcn_ballot_w64(keep && kb < start);
+        if (lane == 0) {
+          misc[wave] = __builtin_popcountll(mask);
+          misc[16 + wave] = __builtin_popcountll(below);
+        }
         __syncthreads();
         int32_t pos = nu, total = 0;
 #pragma unroll
         for (int w = 0; w < 8; w++) {
           pos += w < wave ? misc[w] : 0;
           total += misc[w];
+          first += misc[16 + w];
         }
         pos += __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
@@ -1808,11 +2020,12 @@ __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
         nu += total;
         __syncthreads();
       }
+      first = __builtin_amdgcn_readfirstlane(first < nu ? first : 0);
     }
     const size_t off = (size_t)bh * n * D;
     process_pair<D, BLK, SPARSE, PAD>(plan, grp, q + off, k + off, v + off, o + off,
-                                      lse ? lse + (size_t)bh * n : nullptr, n, my_row, nu, list, c,
-                                      sk, sv, masks);
+                                      lse ? lse + (size_t)bh * n : nullptr, n, my_row, nu, first, list,
+                                      c, sk, sv, masks);
   }
 }
 
@@ -1830,7 +2043,7 @@ static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, v
     // one eight-wave pair workgroup per CU
     static_assert(sizeof(PlanHeader) <= 256, "the plan header is the workspace's first section");
     const PlanView pv = {(uint32_t)wl.params, (uint32_t)wl.coords, (uint32_t)wl.order, (uint32_t)wl.queues,
-                         (uint32_t)(PAD ? wl.masks : 0), (uint32_t)wl.pairs};
+                         (uint32_t)(PAD ? wl.masks : 0), (uint32_t)wl.pairs, (uint32_t)wl.starts};
     hipLaunchKernelGGL((psa_pair_kernel<D, BLK, true, PAD>), dim3(n_wg / 2), dim3(4 * BLK), 0, stream,
                        (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
                        (const uint8_t*)ws, pv, expect, c);
@@ -1894,7 +2107,7 @@ static hipError_t launch_dense_t(const void* q, const void* k, const void* v, vo
     e.nb = nb;
     e.n = n;
     const int32_t grid = queues ? n_wg / 2 : per_xcd * kNumQueues;
-    const PlanView pv = {0, 0, 0, 0, 0, 0};         // the dense workspace is the queue area
+    const PlanView pv = {0, 0, 0, 0, 0, 0, 0};      // the dense workspace is the queue area
     hipLaunchKernelGGL((psa_pair_kernel<D, BLK, false, false>), dim3(grid), dim3(4 * BLK), 0, stream,
                        (const __bf16*)q, (const __bf16*)k, (const __bf16*)v, (__bf16*)o, lse,
                        (const uint8_t*)queues, pv, e, c);

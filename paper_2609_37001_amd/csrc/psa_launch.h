@@ -62,6 +62,10 @@ struct PlanHeader {
 constexpr int kCounterStride = 32;
 constexpr int kQueueCounters = 32;
 constexpr int kQueueWords = kQueueCounters + kNumQueues * kCounterStride;
+// Word of the first line (after the boundaries) counting the finished workgroups of the plan's
+// last kernel at block 128.
+constexpr int kStartsDone = 16;
+static_assert(kStartsDone > kNumQueues && kStartsDone < kQueueCounters, "free word of the first line");
 
 // Workspace of psa_dense_fwd: the queue area alone, rounded up to 256 bytes.
 constexpr size_t kDenseWorkspaceBytes = (sizeof(int32_t) * kQueueWords + 255) / 256 * 256;
@@ -76,6 +80,11 @@ struct WorkspaceLayout {
   size_t queues;    // int32 [kQueueWords]: queue boundaries and pop counters
   size_t sigs;      // uint64 [n_heads][nb]: signature of each query block's kept set
   size_t pairs;     // int2 [n_heads][ceil(nb/2)]: query blocks paired into one work item
+  size_t spans;     // uint32 [batch*n_heads*ceil(nb/2)]: first and last kept non-global key block
+                    // of each pair item (bits 0-15, 16-31; 0xffffffff: none)
+  size_t runspans;  // uint32 [batch*n_heads*ceil(nb/2)]: union of the spans of the items of the
+                    // item's run (its head's range in its queue; a long item alone)
+  size_t starts;    // int32 [batch*n_heads*ceil(nb/2)]: key block each pair item's stream starts at
   size_t masks;     // uint64 [nb][2]: valid positions of each tile (3D only)
   size_t total;
 };
