@@ -937,18 +937,20 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
 // and places the predecessor's position by linear interpolation over the predecessor's span of
 // non-global key blocks.  Items that keep every key block start at block 0 (ascending, as in the
 // dense kernel).  The result depends on the plan only, so runs stay deterministic.
-// One single-wave workgroup per queue; the last workgroup to finish writes the plan header.
-//  1. Start times: the 32 times at which the XCD's workgroups become free are kept sorted over
-//     lanes 0..31; the queue's items are replayed 16 at a time -- they start at the 16 earliest
-//     free times (this differs from taking them one by one only when an item of the group would
-//     end before a later one of the group starts), their workgroups' next free times replace those
-//     lanes, and a bitonic sort over the 32 lanes restores the order.  Each item's start time is
-//     kept in `starts` for step 2.
-//  2. Start blocks: within a run (the items of one head's range in the queue), each item starts
-//     where its predecessor is predicted to be by then: the predecessor's start block advanced by
-//     (its elapsed time / its work) of the run's span, cyclically; a run's first item starts at
-//     its own first non-global block.  These are prefix sums over each run, 64 items at a time.
-// Items that keep every key block start at block 0 (ascending, as in the dense kernel).
+// One 1024-thread workgroup per queue, over tiles of kStartsTile queue entries; the last
+// workgroup to finish writes the plan header.
+//  0. All waves load the tile's items, kept counts and spans into LDS.
+//  1. Start times (wave 0): the 32 times at which the XCD's workgroups become free are kept
+//     sorted over lanes 0..31; the queue's items are replayed 16 at a time -- they start at the
+//     16 earliest free times (this differs from taking them one by one only when an item of the
+//     group would end before a later one of the group starts), their workgroups' next free times
+//     replace those lanes, and a bitonic sort over the 32 lanes restores the order.
+//  2. Start blocks (all waves): within a run (the items of one head's range in the queue), each
+//     item starts where its predecessor is predicted to be by then: the predecessor's start block
+//     advanced by (its elapsed time / its work) of the run's span, cyclically; a run's first item
+//     starts at its own first non-global block.  These are segmented prefix sums: a plain prefix
+//     sum over the tile less its value where the item's run began (a running maximum of the run
+//     starts), the last item's sum carried into the next tile.
 constexpr int kStartGroup = 16;
 constexpr uint32_t kNoSpan = 0xffffffffu;
 
@@ -973,98 +975,132 @@ __device__ __forceinline__ int32_t bitonic_step(int32_t v, int lane) {
   return up ? min(v, other) : max(v, other);
 }
 
-__global__ __launch_bounds__(64) void psa_starts_kernel(
+constexpr int kStartsTile = 2048;
+static_assert(kStartsTile % kStartGroup == 0, "the replay's groups of a queue must not straddle tiles");
+__global__ __launch_bounds__(1024) void psa_starts_kernel(
     const int32_t* __restrict__ counts, const uint32_t* __restrict__ spans,
     const uint32_t* __restrict__ runspans, const int32_t* __restrict__ order,
     int32_t* __restrict__ queues, int32_t* __restrict__ starts, PlanHeader* __restrict__ header,
     PlanHeader done, int32_t np, int32_t nb) {
   constexpr int kSlots = 32;                       // workgroups of one XCD
-  const int lane = threadIdx.x, queue = blockIdx.x;
+  constexpr int kPer = kStartsTile / 1024;         // entries per thread in the loads
+  __shared__ int32_t s_item[kStartsTile], s_cnt[kStartsTile], s_t[kStartsTile];
+  __shared__ uint32_t s_own[kStartsTile], s_run[kStartsTile];
+  __shared__ int32_t s_v[kStartsTile], s_sum[kStartsTile], s_seg[kStartsTile];
+  __shared__ int32_t part[16];
+  __shared__ int32_t c_bh, c_t, c_work, c_acc;     // the entry before the tile
+  __shared__ uint32_t c_run;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, queue = blockIdx.x;
   const int32_t q0 = queues[queue], q1 = queues[queue + 1];
-
-  // 1. Start times (lanes 32..63 hold INT32_MAX and stay in place).
-  int32_t free_at = lane < kSlots ? 0 : INT32_MAX;
-  for (int32_t base = q0; base < q1; base += kStartGroup) {
-    const int gn = min(kStartGroup, q1 - base);
-    const bool mine = lane < gn;
-    const int32_t item = mine ? order[base + lane] : 0;
-    const int32_t work = mine ? counts[item] + kItemOverhead : 0;
-    if (mine) starts[item] = free_at;              // lane i: the i-th earliest free time
-    free_at += work;
-    free_at = bitonic_step<2, 1>(free_at, lane);
-    free_at = bitonic_step<4, 2>(free_at, lane);
-    free_at = bitonic_step<4, 1>(free_at, lane);
-    free_at = bitonic_step<8, 4>(free_at, lane);
-    free_at = bitonic_step<8, 2>(free_at, lane);
-    free_at = bitonic_step<8, 1>(free_at, lane);
-    free_at = bitonic_step<16, 8>(free_at, lane);
-    free_at = bitonic_step<16, 4>(free_at, lane);
-    free_at = bitonic_step<16, 2>(free_at, lane);
-    free_at = bitonic_step<16, 1>(free_at, lane);
-    free_at = bitonic_step<32, 16>(free_at, lane);
-    free_at = bitonic_step<32, 8>(free_at, lane);
-    free_at = bitonic_step<32, 4>(free_at, lane);
-    free_at = bitonic_step<32, 2>(free_at, lane);
-    free_at = bitonic_step<32, 1>(free_at, lane);
-    free_at = lane < kSlots ? free_at : INT32_MAX;
+  if (tid == 0) {
+    c_bh = -1;
+    c_t = 0;
+    c_work = 1;
+    c_acc = 0;
+    c_run = kNoSpan;
   }
-  __threadfence_block();                            // step 2 reads what step 1 wrote
-
-  // 2. Start blocks: segmented prefix sums over the runs, 64 items at a time.
-  int32_t c_bh = -1, c_start = 0, c_work = 1;       // the item before this chunk
-  uint32_t c_run = kNoSpan;
-  int64_t c_acc = 0;                                 // the running sum at that item
-  for (int32_t base = q0; base < q1; base += 64) {
-    const int32_t idx = base + lane;
-    const bool live = idx < q1;
-    const int32_t item = live ? order[idx] : 0;
-    const int32_t bh = item / np;
-    const int32_t cnt = live ? counts[item] : 0;
-    const uint32_t own = live ? spans[item] : kNoSpan;
-    const uint32_t run = live ? runspans[item] : kNoSpan;
-    const int32_t t = live ? starts[item] : 0;
-    // the previous item of the queue
-    int32_t p_bh = __shfl_up(bh, 1), p_t = __shfl_up(t, 1), p_work = __shfl_up(cnt, 1) + kItemOverhead;
-    uint32_t p_run = (uint32_t)__shfl_up((int32_t)run, 1);
-    if (lane == 0) {
-      p_bh = c_bh;
-      p_t = c_start;
-      p_work = c_work;
-      p_run = c_run;
+  int32_t free_at = lane < kSlots ? 0 : INT32_MAX; // wave 0, carried over the tiles
+  for (int32_t t0 = q0; t0 < q1; t0 += kStartsTile) {
+    const int32_t tn = min(kStartsTile, q1 - t0);
+    // 0. loads: every thread issues its item indices, then their counts and spans
+    int32_t it[kPer];
+#pragma unroll
+    for (int r = 0; r < kPer; r++) {
+      const int32_t i = tid + 1024 * r;
+      it[r] = i < tn ? order[t0 + i] : 0;
     }
-    const bool first = p_bh != bh || p_run != run || idx == q0;
-    const int32_t lo = (int32_t)(run & 0xffffu), len = (int32_t)(run >> 16) - lo + 1;
-    int64_t v = 0;
-    if (run != kNoSpan) {
-      if (first)
-        v = own != kNoSpan ? (int64_t)(own & 0xffffu) - lo : 0;
-      else
-        v = (int64_t)min(max(t - p_t, 0), p_work - 1) * len / p_work;
-    }
-    // segmented inclusive scan (a segment starts at `first`; lane 0 continues the carry)
-    int64_t acc = v;
-    bool head = first;
-    if (lane == 0 && !first) acc += c_acc;
-    for (int off = 1; off < 64; off <<= 1) {
-      const int64_t a = __shfl_up(acc, off);
-      const int hs = __shfl_up((int)head, off);
-      if (lane >= off && !head) {
-        acc += a;
-        head = hs != 0;
+#pragma unroll
+    for (int r = 0; r < kPer; r++) {
+      const int32_t i = tid + 1024 * r;
+      if (i < tn) {
+        s_item[i] = it[r];
+        s_cnt[i] = counts[it[r]];
+        s_own[i] = spans[it[r]];
+        s_run[i] = runspans[it[r]];
       }
     }
-    int32_t kb = run == kNoSpan ? 0 : lo + (int32_t)(acc % len);
-    if (cnt >= nb) kb = 0;
-    if (live) starts[item] = kb;
-    // carry: the last live item of the chunk
-    const int lastl = min(64, q1 - base) - 1;
-    c_bh = __shfl(bh, lastl);
-    c_start = __shfl(t, lastl);
-    c_work = __shfl(cnt, lastl) + kItemOverhead;
-    c_run = (uint32_t)__shfl((int32_t)run, lastl);
-    c_acc = __shfl(acc, lastl);
+    __syncthreads();
+    // 1. start times
+    if (wave == 0) {
+      int32_t w_next = lane < kStartGroup && lane < tn ? s_cnt[lane] : 0;
+      for (int32_t g = 0; g < tn; g += kStartGroup) {
+        const int32_t gn = min(kStartGroup, tn - g);
+        const int32_t w = w_next;
+        w_next = lane < kStartGroup && g + kStartGroup + lane < tn ? s_cnt[g + kStartGroup + lane] : 0;
+        if (lane < gn) s_t[g + lane] = free_at;    // lane i: the i-th earliest free time
+        free_at += lane < gn ? w + kItemOverhead : 0;
+        free_at = bitonic_step<2, 1>(free_at, lane);
+        free_at = bitonic_step<4, 2>(free_at, lane);
+        free_at = bitonic_step<4, 1>(free_at, lane);
+        free_at = bitonic_step<8, 4>(free_at, lane);
+        free_at = bitonic_step<8, 2>(free_at, lane);
+        free_at = bitonic_step<8, 1>(free_at, lane);
+        free_at = bitonic_step<16, 8>(free_at, lane);
+        free_at = bitonic_step<16, 4>(free_at, lane);
+        free_at = bitonic_step<16, 2>(free_at, lane);
+        free_at = bitonic_step<16, 1>(free_at, lane);
+        free_at = bitonic_step<32, 16>(free_at, lane);
+        free_at = bitonic_step<32, 8>(free_at, lane);
+        free_at = bitonic_step<32, 4>(free_at, lane);
+        free_at = bitonic_step<32, 2>(free_at, lane);
+        free_at = bitonic_step<32, 1>(free_at, lane);
+        free_at = lane < kSlots ? free_at : INT32_MAX;
+      }
+    }
+    __syncthreads();
+    // 2. each entry's step from its predecessor (v), and where its run began (seg)
+    for (int32_t i = tid; i < tn; i += 1024) {
+      const int32_t bh = s_item[i] / np, t = s_t[i];
+      const uint32_t run = s_run[i], own = s_own[i];
+      int32_t p_bh, p_t, p_work;
+      uint32_t p_run;
+      if (i > 0) {
+        p_bh = s_item[i - 1] / np;
+        p_t = s_t[i - 1];
+        p_work = s_cnt[i - 1] + kItemOverhead;
+        p_run = s_run[i - 1];
+      } else {
+        p_bh = c_bh;
+        p_t = c_t;
+        p_work = c_work;
+        p_run = c_run;
+      }
+      const bool first = p_bh != bh || p_run != run || t0 + i == q0;
+      const int32_t lo = (int32_t)(run & 0xffffu), len = (int32_t)(run >> 16) - lo + 1;
+      int32_t v = 0;
+      if (run != kNoSpan) {
+        if (first)
+          v = own != kNoSpan ? (int32_t)(own & 0xffffu) - lo : 0;
+        else
+          v = min(max(t - p_t, 0), p_work - 1) * len / p_work;   // < 2^13 * 2^13
+      }
+      s_v[i] = v;
+      s_sum[i] = v;
+      s_seg[i] = first ? i : -1;
+    }
+    __syncthreads();
+    const int32_t carry = c_acc;
+    block_scan<false>(s_sum, tn, part);              // exclusive sums
+    block_scan<true>(s_seg, tn, part);               // start of each entry's run, -1: before the tile
+    for (int32_t i = tid; i < tn; i += 1024) {
+      const int32_t seg = s_seg[i];
+      const int32_t acc = s_sum[i] + s_v[i] - (seg >= 0 ? s_sum[seg] : -carry);
+      const uint32_t run = s_run[i];
+      const int32_t lo = (int32_t)(run & 0xffffu), len = (int32_t)(run >> 16) - lo + 1;
+      int32_t kb = run == kNoSpan ? 0 : lo + acc % len;
+      if (s_cnt[i] >= nb) kb = 0;
+      starts[s_item[i]] = kb;
+      if (i == tn - 1) {                             // carry into the next tile
+        c_bh = s_item[i] / np;
+        c_t = s_t[i];
+        c_work = s_cnt[i] + kItemOverhead;
+        c_run = run;
+        c_acc = acc;
+      }
+    }
+    __syncthreads();
   }
-  if (lane == 0) {
+  if (tid == 0) {
     __threadfence();
     if (atomicAdd(&queues[kStartsDone], 1) == kNumQueues - 1) {
       __threadfence();
@@ -1130,7 +1166,7 @@ hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, vo
                      pair_engine(g) ? (const uint32_t*)(ws + wl.spans) : nullptr,
                      pair_engine(g) ? (uint32_t*)(ws + wl.runspans) : nullptr);
   if ((e = hipGetLastError()) != hipSuccess || !pair_engine(g)) return e;
-  hipLaunchKernelGGL(psa_starts_kernel, dim3(kNumQueues), dim3(64), 0, stream, (const int32_t*)counts,
+  hipLaunchKernelGGL(psa_starts_kernel, dim3(kNumQueues), dim3(1024), 0, stream, (const int32_t*)counts,
                      (const uint32_t*)(ws + wl.spans), (const uint32_t*)(ws + wl.runspans),
                      (const int32_t*)(ws + wl.order), (int32_t*)(ws + wl.queues), (int32_t*)(ws + wl.starts),
                      (PlanHeader*)(ws + wl.header), plan_header(g, batch, n_heads), per_head, g.nb);
