@@ -116,6 +116,34 @@ __device__ __forceinline__ int wave_sum(int v) {
   return v;
 }
 
+// Wave-wide sum (OP 0), minimum (1) or maximum (2) in every lane, without LDS: DPP moves
+// within the 16-lane rows, then the gfx950 permlane swaps across rows.
+template <int OP>
+__device__ __forceinline__ int32_t wave_reduce(int32_t v) {
+  auto op = [](int32_t a, int32_t b) { return OP == 0 ? a + b : (OP == 1 ? min(a, b) : max(a, b)); };
+  v = op(v, __builtin_amdgcn_update_dpp(v, v, 0xb1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
+  v = op(v, __builtin_amdgcn_update_dpp(v, v, 0x4e, 0xf, 0xf, false));   // quad_perm 2,3,0,1
+  v = op(v, __builtin_amdgcn_update_dpp(v, v, 0x124, 0xf, 0xf, false));  // row_ror:4
+  v = op(v, __builtin_amdgcn_update_dpp(v, v, 0x128, 0xf, 0xf, false));  // row_ror:8
+  const auto r16 = __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+  v = op((int32_t)r16[0], (int32_t)r16[1]);                               // lanes l, l ^ 16
+  const auto r32 = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
+  return op((int32_t)r32[0], (int32_t)r32[1]);                            // lanes l, l ^ 32
+}
+
+// Inclusive prefix sum over the lanes of a wave: shifted DPP adds within each row, then the
+// totals of the rows below added from scalar reads of their last lanes.
+__device__ __forceinline__ int32_t wave_incl_sum(int32_t v, int lane) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);         // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);         // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);         // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);         // row_shr:8
+  const int32_t r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
+                r2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane >> 4;
+  return v + (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
+}
+
 // ---------------------------------------------------------------------------------------------
 // Block map (psa_build_blockmap).
 // ---------------------------------------------------------------------------------------------
@@ -706,8 +734,10 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
   for (int32_t i = tid; i < kScheduleWaves * kWorkClasses; i += 1024) (&hist[0][0])[i] = 0;
   __syncthreads();
   constexpr int kLoads = 4;                 // loads in flight per lane in the sweeps below
+  // Sums of one pair's work stay below 2^31: at most PSA_MAX_BLOCKS items of at most
+  // PSA_MAX_BLOCKS + kItemOverhead tiles.
   for (int32_t bh = wave; bh < n_bh; bh += kScheduleWaves) {
-    int64_t s = 0;
+    int32_t s = 0;
     int32_t mx = 0;
     for (int32_t q0 = lane; q0 < nb; q0 += 64 * kLoads) {
       int32_t c[kLoads];
@@ -719,10 +749,8 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
         mx = max(mx, c[j]);
       }
     }
-    for (int off = 32; off > 0; off >>= 1) {
-      s += __shfl_xor(s, off);
-      mx = max(mx, __shfl_xor(mx, off));
-    }
+    s = wave_reduce<0>(s);
+    mx = wave_reduce<2>(mx);
     if (lane == 0) {
       total[bh] = s;
       atomicAdd(&all_work, (uint64_t)s);
@@ -739,15 +767,15 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
   if (any_long) {
     // Work of each pair without its long items.
     for (int32_t bh = wave; bh < n_bh; bh += kScheduleWaves) {
-      int64_t s = 0;
+      int32_t s = 0;
       for (int32_t q0 = lane; q0 < nb; q0 += 64 * kLoads) {
         int64_t w[kLoads];
 #pragma unroll
         for (int j = 0; j < kLoads; j++) w[j] = q0 + 64 * j < nb ? work_of(bh * nb + q0 + 64 * j) : 0;
 #pragma unroll
-        for (int j = 0; j < kLoads; j++) s += w[j] * n > long_above ? 0 : w[j];
+        for (int j = 0; j < kLoads; j++) s += w[j] * n > long_above ? 0 : (int32_t)w[j];
       }
-      for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+      s = wave_reduce<0>(s);
       if (lane == 0) total[bh] = s;
     }
     __syncthreads();
@@ -765,25 +793,21 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
   for (int32_t r = wave; r < n_bh; r += kScheduleWaves) {
     const int32_t bh = by_rank[r];
     const int64_t head_total = total[bh];
-    int64_t base = 0;
+    int32_t base = 0;
     int32_t next = 1;                       // next boundary to place
     if (lane == 0) bounds[r][0] = 0;
     for (int32_t g0 = 0; g0 < nb && next < kNumQueues; g0 += 64 * kLoads) {
-      int64_t wv[kLoads];
+      int32_t wv[kLoads];
 #pragma unroll
       for (int j = 0; j < kLoads; j++) {
         const int32_t qb = g0 + 64 * j + lane;
-        wv[j] = qb < nb && !is_long(bh * nb + qb) ? work_of(bh * nb + qb) : 0;
+        wv[j] = qb < nb && !is_long(bh * nb + qb) ? (int32_t)work_of(bh * nb + qb) : 0;
       }
 #pragma unroll
       for (int j = 0; j < kLoads; j++) {
         const int32_t q0 = g0 + 64 * j, qb = q0 + lane;
-        const int64_t w = wv[j];
-        int64_t incl = w;                   // inclusive prefix over the wave
-        for (int off = 1; off < 64; off <<= 1) {
-          const int64_t t = __shfl_up(incl, off);
-          if (lane >= off) incl += t;
-        }
+        const int32_t w = wv[j];
+        const int32_t incl = wave_incl_sum(w, lane);        // inclusive prefix over the wave
         const int64_t excl = base + incl - w;
         // range x starts at the first block whose preceding work reaches x/Q of the head
         while (next < kNumQueues) {
@@ -794,7 +818,7 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
           if (lane == 0) bounds[r][next] = (uint16_t)first;
           next++;
         }
-        base += __shfl(incl, 63);
+        base += __builtin_amdgcn_readlane(incl, 63);
       }
     }
     for (; next < kNumQueues; next++)
@@ -891,30 +915,52 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
     }
     __builtin_amdgcn_wave_barrier();
   }
-  for (int32_t pair = wave; pair < n_bh * kNumQueues; pair += kScheduleWaves) {
-    const int32_t r = pair / kNumQueues, x = pair - r * kNumQueues;
-    const int32_t item0 = by_rank[r] * nb, end = bounds[r][x + 1];
+  // Each wave takes ranges W, W + 16, ...; the count and span of the first 64 items of the next
+  // range are loaded while the current one is written.
+  const int32_t n_ranges = n_bh * kNumQueues;
+  auto head_of = [&](int32_t range, int32_t& cnt, uint32_t& span) {
+    cnt = 0;
+    span = 0xffffffffu;
+    if (range >= n_ranges) return;
+    const int32_t r = range / kNumQueues, x = range - r * kNumQueues;
+    const int32_t qb = bounds[r][x] + lane;
+    if (qb >= bounds[r][x + 1]) return;
+    if (any_long) cnt = counts[by_rank[r] * nb + qb];
+    if (runspans) span = spans[by_rank[r] * nb + qb];
+  };
+  int32_t next_cnt;
+  uint32_t next_span;
+  head_of(wave, next_cnt, next_span);
+  for (int32_t range = wave; range < n_ranges; range += kScheduleWaves) {
+    const int32_t head_cnt = next_cnt;
+    const uint32_t head_span = next_span;
+    head_of(range + kScheduleWaves, next_cnt, next_span);
+    const int32_t r = range / kNumQueues, x = range - r * kNumQueues;
+    const int32_t item0 = by_rank[r] * nb, begin = bounds[r][x], end = bounds[r][x + 1];
     int32_t* dst = order + qstart[x] + qoff[r][x];
-    uint32_t lo = 0xffffu, hi = 0;
-    for (int32_t qb = bounds[r][x] + lane; __builtin_amdgcn_readfirstlane(qb - lane) < end; qb += 64) {
-      const bool keep = qb < end && !is_long(item0 + qb);
+    int32_t lo = 0xffff, hi = 0;
+    bool head_keep = false;
+    for (int32_t qb = begin + lane; __builtin_amdgcn_readfirstlane(qb - lane) < end; qb += 64) {
+      const bool head = qb - lane == begin;
+      const int32_t cnt = head ? head_cnt : (any_long && qb < end ? counts[item0 + qb] : 0);
+      const uint32_t span = head ? head_span : (runspans && qb < end ? spans[item0 + qb] : 0xffffffffu);
+      const bool keep = qb < end && !(any_long && ((int64_t)cnt + kItemOverhead) * n > long_above);
+      if (head) head_keep = keep;
       const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
       if (keep) dst[__builtin_popcountll(mask & ((1ull << lane) - 1))] = item0 + qb;
       dst += __builtin_popcountll(mask);
-      if (runspans && keep && spans[item0 + qb] != 0xffffffffu) {
-        lo = min(lo, spans[item0 + qb] & 0xffffu);
-        hi = max(hi, spans[item0 + qb] >> 16);
+      if (keep && span != 0xffffffffu) {
+        lo = min(lo, (int32_t)(span & 0xffffu));
+        hi = max(hi, (int32_t)(span >> 16));
       }
     }
     if (runspans) {
       // the run's span: the union of its items' spans of non-global blocks
-      for (int off = 32; off > 0; off >>= 1) {
-        lo = min(lo, (uint32_t)__shfl_xor((int32_t)lo, off));
-        hi = max(hi, (uint32_t)__shfl_xor((int32_t)hi, off));
-      }
-      const uint32_t run = lo > hi ? 0xffffffffu : (lo | (hi << 16));
-      for (int32_t qb = bounds[r][x] + lane; qb < end; qb += 64)
-        if (!is_long(item0 + qb)) runspans[item0 + qb] = run;
+      lo = wave_reduce<1>(lo);
+      hi = wave_reduce<2>(hi);
+      const uint32_t run = lo > hi ? 0xffffffffu : ((uint32_t)lo | ((uint32_t)hi << 16));
+      for (int32_t qb = begin + lane; qb < end; qb += 64)
+        if (qb - lane == begin ? head_keep : !is_long(item0 + qb)) runspans[item0 + qb] = run;
     }
   }
   if (tid <= kNumQueues) queues[tid] = qstart[tid];
