@@ -38,6 +38,7 @@
 #include <stdint.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "psa_launch.h"
 
@@ -129,6 +130,20 @@ __device__ __forceinline__ int32_t wave_reduce(int32_t v) {
   v = op((int32_t)r16[0], (int32_t)r16[1]);                               // lanes l, l ^ 16
   const auto r32 = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
   return op((int32_t)r32[0], (int32_t)r32[1]);                            // lanes l, l ^ 32
+}
+
+// Lane i receives lane i ^ m of x (m = 1, 2, 4, 8 by DPP within a 16-lane row; 16 by a shuffle).
+template <int M>
+__device__ __forceinline__ int32_t lane_xor(int32_t x, int lane) {
+  if constexpr (M == 1) return __builtin_amdgcn_update_dpp(x, x, 0xb1, 0xf, 0xf, false);  // quad_perm 1,0,3,2
+  if constexpr (M == 2) return __builtin_amdgcn_update_dpp(x, x, 0x4e, 0xf, 0xf, false);  // quad_perm 2,3,0,1
+  if constexpr (M == 4) {
+    const int32_t fwd = __builtin_amdgcn_update_dpp(x, x, 0x104, 0xf, 0xf, false);      // row_shl:4
+    const int32_t bwd = __builtin_amdgcn_update_dpp(x, x, 0x114, 0xf, 0xf, false);      // row_shr:4
+    return (lane & 4) ? bwd : fwd;
+  }
+  if constexpr (M == 8) return __builtin_amdgcn_update_dpp(x, x, 0x128, 0xf, 0xf, false); // row_ror:8
+  return __shfl_xor(x, M);
 }
 
 // Inclusive prefix sum over the lanes of a wave: shifted DPP adds within each row, then the
@@ -549,7 +564,7 @@ __global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __res
   __shared__ int32_t run[kPairSort];          // start of each sorted position's run
   __shared__ int16_t partner[kPairSort];      // by row: partner (first row), -1 single, -2 second
   __shared__ int32_t part[16];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
   const uint64_t* sg = sigs + (size_t)blockIdx.x * nb;
   int32_t n2 = 1;
   while (n2 < nb) n2 <<= 1;
@@ -558,9 +573,13 @@ __global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __res
     partner[i] = -3;
   }
   __syncthreads();
-  auto sort_keys = [&]() {                                // bitonic sort of key[0 .. n2), ascending
-    for (int32_t k = 2; k <= n2; k <<= 1)
-      for (int32_t j = k >> 1; j > 0; j >>= 1) {
+  // Bitonic sort of key[0 .. n2), ascending.  Partners 64 or more apart meet in LDS (one
+  // barrier per step); the steps of a stage with partners less than 64 apart run inside each
+  // wave, on registers exchanged across lanes, with one barrier for all of them.
+  auto sort_keys = [&]() {
+    for (int32_t k = 2; k <= n2; k <<= 1) {
+      int32_t j = k >> 1;
+      for (; j >= 64; j >>= 1) {
         for (int32_t i = tid; i < n2; i += 1024) {
           const int32_t ixj = i ^ j;
           if (ixj > i) {
@@ -573,6 +592,26 @@ __global__ __launch_bounds__(1024) void psa_pairing_kernel(const uint64_t* __res
         }
         __syncthreads();
       }
+      for (int32_t i = tid; i < n2; i += 1024) {        // n2 < 64, or whole waves
+        uint64_t x = key[i];
+        const bool up = (i & k) == 0;
+        auto step = [&](auto m) {
+          constexpr int M = decltype(m)::value;
+          if (M > j) return;
+          const uint64_t y = ((uint64_t)(uint32_t)lane_xor<M>((int32_t)(x >> 32), lane) << 32) |
+                             (uint32_t)lane_xor<M>((int32_t)(uint32_t)x, lane);
+          x = (((i & M) == 0) == up) ? min(x, y) : max(x, y);
+        };
+        step(std::integral_constant<int, 32>());
+        step(std::integral_constant<int, 16>());
+        step(std::integral_constant<int, 8>());
+        step(std::integral_constant<int, 4>());
+        step(std::integral_constant<int, 2>());
+        step(std::integral_constant<int, 1>());
+        key[i] = x;
+      }
+      __syncthreads();
+    }
   };
   sort_keys();
   auto row_of = [&](int32_t i) { return (int32_t)(key[i] & 8191u); };
@@ -999,20 +1038,6 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
 //     starts), the last item's sum carried into the next tile.
 constexpr int kStartGroup = 16;
 constexpr uint32_t kNoSpan = 0xffffffffu;
-
-// Lane i receives lane i ^ m of x (m = 1, 2, 4, 8 by DPP within a 16-lane row; 16 by a shuffle).
-template <int M>
-__device__ __forceinline__ int32_t lane_xor(int32_t x, int lane) {
-  if constexpr (M == 1) return __builtin_amdgcn_update_dpp(x, x, 0xb1, 0xf, 0xf, false);  // quad_perm 1,0,3,2
-  if constexpr (M == 2) return __builtin_amdgcn_update_dpp(x, x, 0x4e, 0xf, 0xf, false);  // quad_perm 2,3,0,1
-  if constexpr (M == 4) {
-    const int32_t fwd = __builtin_amdgcn_update_dpp(x, x, 0x104, 0xf, 0xf, false);      // row_shl:4
-    const int32_t bwd = __builtin_amdgcn_update_dpp(x, x, 0x114, 0xf, 0xf, false);      // row_shr:4
-    return (lane & 4) ? bwd : fwd;
-  }
-  if constexpr (M == 8) return __builtin_amdgcn_update_dpp(x, x, 0x128, 0xf, 0xf, false); // row_ror:8
-  return __shfl_xor(x, M);
-}
 
 template <int K, int H>
 __device__ __forceinline__ int32_t bitonic_step(int32_t v, int lane) {
