@@ -243,6 +243,27 @@ int32_t persistent_workgroups() {
   return 2 * cus;
 }
 
+// The run of a plan; `rearm` = false right after the plan's own kernels, which leave the queue
+// counters at zero.
+psa_status_t run_planned(const void* q, const void* k, const void* v, void* o, int32_t batch,
+                         int32_t n_heads, int32_t head_dim, psa_grid_t grid, int32_t block,
+                         float softmax_scale, void* workspace, size_t workspace_bytes, float* lse,
+                         hipStream_t stream, bool rearm) {
+  psa_status_t s = check_tensors(q, k, v, o, lse);
+  if (s != PSA_OK) return s;
+  s = check_attention_shape(batch, n_heads, head_dim, block);
+  if (s != PSA_OK) return s;
+  psa::Geometry g;
+  psa::WorkspaceLayout wl;
+  s = check_plan(batch, n_heads, grid, block, workspace, workspace_bytes, &g, &wl);
+  if (s != PSA_OK) return s;
+  const float c = softmax_scale * 1.4426950408889634f;
+  hipError_t e = psa::launch_sparse(q, k, v, o, lse, batch, n_heads, head_dim, g, c, workspace, wl,
+                                    persistent_workgroups(), stream, rearm);
+  if (e != hipSuccess) return hip_fail(e, "psa_attention_run kernel launch");
+  return PSA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -395,19 +416,8 @@ psa_status_t psa_attention_run(const void* q, const void* k, const void* v, void
                                int32_t batch, int32_t n_heads, int32_t head_dim, psa_grid_t grid,
                                int32_t block, float softmax_scale, void* workspace,
                                size_t workspace_bytes, float* lse, hipStream_t stream) {
-  psa_status_t s = check_tensors(q, k, v, o, lse);
-  if (s != PSA_OK) return s;
-  s = check_attention_shape(batch, n_heads, head_dim, block);
-  if (s != PSA_OK) return s;
-  psa::Geometry g;
-  psa::WorkspaceLayout wl;
-  s = check_plan(batch, n_heads, grid, block, workspace, workspace_bytes, &g, &wl);
-  if (s != PSA_OK) return s;
-  const float c = softmax_scale * 1.4426950408889634f;
-  hipError_t e = psa::launch_sparse(q, k, v, o, lse, batch, n_heads, head_dim, g, c, workspace, wl,
-                                    persistent_workgroups(), stream);
-  if (e != hipSuccess) return hip_fail(e, "psa_attention_run kernel launch");
-  return PSA_OK;
+  return run_planned(q, k, v, o, batch, n_heads, head_dim, grid, block, softmax_scale, workspace,
+                     workspace_bytes, lse, stream, true);
 }
 
 psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void* o,
@@ -422,8 +432,8 @@ psa_status_t psa_attention_fwd(const void* q, const void* k, const void* v, void
   s = psa_attention_plan(batch, n_heads, grid, block, params, workspace, workspace_bytes,
                          kept_per_row, stream);
   if (s != PSA_OK) return s;
-  return psa_attention_run(q, k, v, o, batch, n_heads, head_dim, grid, block, softmax_scale,
-                           workspace, workspace_bytes, lse, stream);
+  return run_planned(q, k, v, o, batch, n_heads, head_dim, grid, block, softmax_scale, workspace,
+                     workspace_bytes, lse, stream, false);
 }
 
 psa_status_t psa_attention_fwd_noalloc(const void* q, const void* k, const void* v, void* o,

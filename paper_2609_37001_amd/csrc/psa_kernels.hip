@@ -2140,12 +2140,14 @@ template <int D, int BLK, bool PAD>
 static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, void* o,
                                   float* lse, const PlanHeader& expect, float c,
                                   void* workspace, const WorkspaceLayout& wl, int32_t n_wg,
-                                  hipStream_t stream) {
+                                  hipStream_t stream, bool rearm) {
   char* ws = (char*)workspace;
-  hipLaunchKernelGGL(psa_rearm_kernel, dim3(1), dim3(64), 0, stream, (int32_t*)(ws + wl.queues),
-                     (const PlanHeader*)(ws + wl.header), expect);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (rearm) {
+    hipLaunchKernelGGL(psa_rearm_kernel, dim3(1), dim3(64), 0, stream, (int32_t*)(ws + wl.queues),
+                       (const PlanHeader*)(ws + wl.header), expect);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if constexpr (BLK == 128) {
     // one eight-wave pair workgroup per CU
     static_assert(sizeof(PlanHeader) <= 256, "the plan header is the workspace's first section");
@@ -2168,27 +2170,27 @@ static hipError_t launch_sparse_t(const void* q, const void* k, const void* v, v
 hipError_t launch_sparse(const void* q, const void* k, const void* v, void* o, float* lse,
                          int32_t batch, int32_t n_heads, int32_t head_dim, const Geometry& g,
                          float c, void* workspace, const WorkspaceLayout& wl, int32_t n_wg,
-                         hipStream_t stream) {
+                         hipStream_t stream, bool rearm) {
   const PlanHeader e = plan_header(g, batch, n_heads);
   if (g.pbt > 0) {
     if (head_dim == 128 && g.block == 128)
-      return launch_sparse_t<128, 128, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+      return launch_sparse_t<128, 128, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
     if (head_dim == 64 && g.block == 64)
-      return launch_sparse_t<64, 64, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+      return launch_sparse_t<64, 64, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
     if (head_dim == 128 && g.block == 64)
-      return launch_sparse_t<128, 64, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+      return launch_sparse_t<128, 64, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
     if (head_dim == 64 && g.block == 128)
-      return launch_sparse_t<64, 128, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+      return launch_sparse_t<64, 128, true>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
     return hipErrorInvalidValue;
   }
   if (head_dim == 128 && g.block == 128)
-    return launch_sparse_t<128, 128, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<128, 128, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
   if (head_dim == 64 && g.block == 64)
-    return launch_sparse_t<64, 64, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<64, 64, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
   if (head_dim == 128 && g.block == 64)
-    return launch_sparse_t<128, 64, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<128, 64, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
   if (head_dim == 64 && g.block == 128)
-    return launch_sparse_t<64, 128, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream);
+    return launch_sparse_t<64, 128, false>(q, k, v, o, lse, e, c, workspace, wl, n_wg, stream, rearm);
   return hipErrorInvalidValue;
 }
 

@@ -128,7 +128,7 @@ hipError_t launch_schedule(const Geometry& g, int32_t batch, int32_t n_heads, vo
 hipError_t launch_sparse(const void* q, const void* k, const void* v, void* o, float* lse,
                          int32_t batch, int32_t n_heads, int32_t head_dim, const Geometry& g,
                          float scale_log2, void* workspace, const WorkspaceLayout& wl,
-                         int32_t n_workgroups, hipStream_t stream);
+                         int32_t n_workgroups, hipStream_t stream, bool rearm = true);
 
 // queues: the int32 [kQueueWords] queue area of a dense workspace (persistent grid of
 // n_workgroups one-row workgroups), or nullptr (one workgroup per work item).
