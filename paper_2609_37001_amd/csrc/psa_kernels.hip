@@ -1012,15 +1012,14 @@ __global__ __launch_bounds__(1024) void psa_schedule_kernel(const int32_t* __res
   }
 }
 
-// Where each pair item's K/V stream starts (one wave per work queue).  The workgroups of one XCD
-// share its L2, and a K/V block stays there for only about two block steps of the XCD's 32
-// workgroups; so a block is reused only when the items in flight on the XCD read it at nearly
-// the same time.  Each item therefore starts its cyclic walk over its key blocks where the item
-// started just before it on the same queue is predicted to be by then: this wave replays the
-// queue with 32 workgroups taking items as they become free (work = kept blocks + item overhead,
-// the schedule's estimate), keeping the 32 times at which they become free sorted over its lanes,
-// and places the predecessor's position by linear interpolation over the predecessor's span of
-// non-global key blocks.  Items that keep every key block start at block 0 (ascending, as in the
+// Where each pair item's K/V stream starts.  The workgroups of one XCD share its L2, and a K/V
+// block stays there for only about two block steps of the XCD's 32 workgroups; so a block is
+// reused only when the items in flight on the XCD read it at nearly the same time.  Each item
+// therefore starts its cyclic walk over its key blocks where the item started just before it on
+// the same queue is predicted to be by then: the queue is replayed with 32 workgroups taking
+// items as they become free (work = kept blocks + item overhead, the schedule's estimate), and
+// the predecessor's position is placed by linear interpolation over the span of non-global key
+// blocks of their run.  Items that keep every key block start at block 0 (ascending, as in the
 // dense kernel).  The result depends on the plan only, so runs stay deterministic.
 // One 1024-thread workgroup per queue, over tiles of kStartsTile queue entries; the last
 // workgroup to finish writes the plan header.
