@@ -51,6 +51,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define PSA_LDS __attribute__((address_space(3)))
 
@@ -1910,6 +1911,43 @@ __device__ __forceinline__ void store_rows(const WaveState<D, BLK>& st, __bf16* 
   }
 }
 
+// The same through LDS: the wave's 32 rows are staged row-major in `stage` (32 x 2D bytes of LDS
+// no other wave touches; 16-byte chunks XOR-swizzled by the row), then stored as whole rows, 16
+// bytes per lane, so that each store covers 64 x 16 contiguous bytes of O instead of 8 bytes in
+// each of 32 rows.  row0 = the wave's first row; lane l holds row row0 + (l & 31).
+template <int D, int BLK>
+__device__ __forceinline__ void store_rows_staged(const WaveState<D, BLK>& st, __bf16* __restrict__ oh,
+                                                  float* __restrict__ lseh, int row0, int n, int lane,
+                                                  uint32_t stage) {
+  using T = Tile<D, BLK>;
+  constexpr int RB = 2 * D;                   // bytes per row
+  constexpr int C16 = RB / 16;                // 16-byte chunks per row
+  // The lane's addresses are formed here, not hoisted out of the item loop into registers that
+  // would stay live across the block loop.
+  asm volatile("" : "+v"(lane));
+  const int h = lane >> 5, r = lane & 31;
+  const float lsum = pair_sum(st.l);
+  const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+#pragma unroll
+  for (int dt = 0; dt < T::DT; dt++)
+#pragma unroll
+    for (int a = 0; a < 4; a++) {
+      const f32x4 v = {st.o[dt][4 * a] * inv, st.o[dt][4 * a + 1] * inv,
+                       st.o[dt][4 * a + 2] * inv, st.o[dt][4 * a + 3] * inv};
+      const int chunk = (4 * dt + a) ^ (r & (C16 - 1));        // columns 8 (4 dt + a) + 4 h ...
+      *(PSA_LDS bf16x4*)(uintptr_t)(stage + r * RB + chunk * 16 + 8 * h) = __builtin_convertvector(v, bf16x4);
+    }
+#pragma unroll 2
+  for (int j = 0; j < 32 * C16 / 64; j++) {
+    const int idx = 64 * j + lane, rr = idx / C16, c = idx % C16;
+    const u32x4 val = *(PSA_LDS u32x4*)(uintptr_t)(stage + rr * RB + ((c ^ (rr & (C16 - 1))) * 16));
+    if (row0 + rr < n) *(u32x4*)(oh + (size_t)(row0 + rr) * D + 8 * c) = val;
+  }
+  if (lseh && h == 0 && row0 + r < n)
+    lseh[row0 + r] = lsum > 0.0f ? (st.m + __builtin_log2f(lsum)) * 0.69314718055994530942f
+                                 : -__builtin_inff();
+}
+
 // Entry i of a pair's block stream: key block in bits 0-12, kept by the first row (bit 13) and
 // by the second row (bit 14).
 constexpr int kEntryRowShift = 13;
@@ -1939,23 +1977,6 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
   const int h = lane >> 5, r32 = lane & 31;
   const int row = my_row * BLK + gw * 32 + r32;
 
-  WaveState<D, BLK> st;
-  if (my_row >= 0) {
-    const bf16x8* src = (const bf16x8*)(qh + (size_t)min(row, n - 1) * D) + h;
-#pragma unroll
-    for (int cc = 0; cc < T::DC; cc++) st.q[cc] = src[2 * cc];
-#pragma unroll
-    for (int cc = 0; cc < T::DC; cc++)
-      st.q[cc] = __builtin_convertvector(__builtin_convertvector(st.q[cc], f32x8) * c, bf16x8);
-#pragma unroll
-    for (int cc = 0; cc < T::DC; cc++) asm volatile("" ::"v"(st.q[cc]));
-  }
-  st.m = -__builtin_inff();
-  st.l = 0.0f;
-  st.negm = (f32x16){};
-#pragma unroll
-  for (int dt = 0; dt < T::DT; dt++) st.o[dt] = (f32x16){};
-
   // Entry i of the stream: list entry first + i, cyclically.
   auto entry = [&](int i) {
     if constexpr (SPARSE) {
@@ -1973,10 +1994,39 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
     issue_block8<D, BLK>(plan, vh, lds_address(sv[buf]), lds_address(sv[buf]) + HALF, kb, n);
   };
   int e = 0;
-  if (nu > 0) {
-    e = entry(0);
-    issue_k(0, e & kEntryBlockMask);
-    issue_v(0, e & kEntryBlockMask);
+  // Sparse: the first block's loads go out before the Q loads, so that the two latencies overlap
+  // at the start of the item (dense: after them; the other order measured slower there).
+  if constexpr (SPARSE) {
+    if (nu > 0) {
+      e = entry(0);
+      issue_k(0, e & kEntryBlockMask);
+      issue_v(0, e & kEntryBlockMask);
+    }
+  }
+
+  WaveState<D, BLK> st;
+  if (my_row >= 0) {
+    const bf16x8* src = (const bf16x8*)(qh + (size_t)min(row, n - 1) * D) + h;
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++) st.q[cc] = src[2 * cc];
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++)
+      st.q[cc] = __builtin_convertvector(__builtin_convertvector(st.q[cc], f32x8) * c, bf16x8);
+#pragma unroll
+    for (int cc = 0; cc < T::DC; cc++) asm volatile("" ::"v"(st.q[cc]));
+  }
+  st.m = -__builtin_inff();
+  st.l = 0.0f;
+  st.negm = (f32x16){};
+#pragma unroll
+  for (int dt = 0; dt < T::DT; dt++) st.o[dt] = (f32x16){};
+
+  if constexpr (!SPARSE) {
+    if (nu > 0) {
+      e = entry(0);
+      issue_k(0, e & kEntryBlockMask);
+      issue_v(0, e & kEntryBlockMask);
+    }
   }
   for (int i = 0; i < nu; i++) {
     const int kb = e & kEntryBlockMask;
@@ -2016,7 +2066,17 @@ __device__ __forceinline__ void process_pair(const DmaPlan8<D, BLK>& plan, int g
       issue_v((i + 1) & 1, kbn);
     }
   }
-  if (my_row >= 0) store_rows<D, BLK>(st, oh, lseh, row, n, lane);
+  if constexpr (SPARSE) {
+    // The buffer of block nu - 2 (every wave passed the barrier of block nu - 1) stages the
+    // output: 8 KB per wave, K half for group 0, V half for group 1.
+    if (my_row >= 0) {
+      static_assert(4 * 32 * 2 * D <= T::BYTES, "a wave's rows fit its share of a free buffer");
+      const uint32_t stage = lds_address(grp == 0 ? sk[nu & 1] : sv[nu & 1]) + gw * (32 * 2 * D);
+      store_rows_staged<D, BLK>(st, oh, lseh, my_row * BLK + gw * 32, n, lane, stage);
+    }
+  } else {
+    if (my_row >= 0) store_rows<D, BLK>(st, oh, lseh, row, n, lane);
+  }
 }
 
 // SPARSE: persistent, one workgroup per CU popping pair items from the plan's queues.  Dense: the
