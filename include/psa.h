@@ -153,7 +153,8 @@ psa_status_t psa_attention_run(const void* q, const void* k, const void* v, void
                                size_t workspace_bytes, float* lse, hipStream_t stream);
 
 /* PSA block-sparse attention forward (Algorithm 2): o = softmax(scale * q k^T restricted to the
- * kept blocks of each head) v.  Equivalent to psa_attention_plan followed by psa_attention_run.
+ * kept blocks of each head) v.  Equivalent to psa_attention_plan followed by psa_attention_run
+ * (without the run's re-arm kernel: the plan's own kernels leave the queue counters armed).
  *   q, k, v, o     device bf16 [batch][n_heads][N][head_dim]; N = frames*height*width + n_text
  *   head_dim       64 or 128;  block: 64 or 128 (query and key block size, the tile size)
  *   params         host [n_heads]; the same M for every batch element
