@@ -46,3 +46,26 @@ def test_sweep_sampled(target):
         od = psa.dense_fwd(q, k, v, cfg.block, cfg.scale)
         gu.torch().cuda.synchronize()
         assert gu.torch().equal(o, od)
+
+
+def test_batch_two_plan_tiles():
+    """Wan 2.1 14B with batch 2: 23,680 pair items, 2,710-3,606 per queue, so the plan's
+    start-block kernel stages each queue in two of its 2,048-entry tiles (one at batch 1).
+    Sampled rows of both batch elements against the oracle."""
+    import dataclasses
+    from workloads.inputs import make_qkv
+    torch = gu.torch()
+    cfg = dataclasses.replace(get_config("wan14b"), batch=2)
+    params = gu.params_of("wan14b")
+    q, k, v = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to("cuda:0")
+               for x in make_qkv(cfg, workers=16))
+    o = torch.full_like(q, float("nan"))
+    o, lse = psa.attention_fwd(q, k, v, gu.grid_of(cfg), cfg.block, params, cfg.scale, out=o,
+                               return_lse=True)
+    torch.cuda.synchronize()
+    del q, k, v
+    assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).logical_or(lse == -np.inf).all())
+    bmap = gu.oracle_map(cfg, params)
+    picks = gu.sample_blocks(cfg, bmap, n_random=3)
+    for b in range(cfg.batch):
+        gu.compare_rows(cfg, params, bmap, o, lse, picks, batch=b).check("wan14b batch element %d:" % b)
