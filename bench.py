@@ -305,7 +305,8 @@ def utilisation_rows(sq_dir, tcc_dir, trace_dir, label):
         cyc = a["GRBM_GUI_ACTIVE"] / 8.0
         rows.append("| %s | %s | %.2f | %.2f | %.3f | %.1f | %.2f | %.3f | %.0f | %.3f |" % (
             label, k, t * 1e3, cyc / t / 1e9, a["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * 1024),
-            a["SQ_VALU_MFMA_BUSY_CYCLES"] / a["SQ_INSTS_MFMA"], a["SQ_INSTS_VALU"] / a["SQ_INSTS_MFMA"],
+            a["SQ_VALU_MFMA_BUSY_CYCLES"] / a["SQ_INSTS_MFMA"],
+            (a["SQ_INSTS_VALU"] - a["SQ_INSTS_MFMA"]) / a["SQ_INSTS_MFMA"],   # SQ_INSTS_VALU counts MFMAs
             a["SQ_ACTIVE_INST_VALU"] * 4 / (cyc * 1024), a["SQ_LDS_BANK_CONFLICT"],
             b["TCC_HIT_sum"] / (b["TCC_HIT_sum"] + b["TCC_MISS_sum"])))
     return rows
@@ -376,7 +377,7 @@ WAIT_HEADER = ("| workload | kernel | waves per SIMD | executing | waiting for a
 
 
 UTIL_HEADER = ("| workload | kernel | ms (trace) | clock GHz | MFMA busy | MFMA cycles per MFMA | "
-               "VALU insts per MFMA | VALU active | LDS bank-conflict cycles | L2 hit |\n"
+               "other VALU insts per MFMA | VALU active | LDS bank-conflict cycles | L2 hit |\n"
                "|---|---|---|---|---|---|---|---|---|---|")
 
 
