@@ -73,6 +73,8 @@ def test_kernel_table_and_utilisation(tmp_path):
     row = rows[0]
     cells = [c.strip() for c in row.strip("|").split("|")]
     assert cells[2:6] == ["100.00", "1.90", "0.500", "32.0"] and cells[-1] == "0.900"
+    # SQ_INSTS_VALU counts the MFMAs: cyc * 64 VALU over cyc * 16 MFMA = 4 per MFMA, 3 others
+    assert cells[6] == "3.00"
 
 
 def test_hbm_and_wait_summaries(tmp_path):
